@@ -1,0 +1,190 @@
+"""ctypes wrapper of the fp64 CPU oracle (``som_oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the
+benchmark's CPU-baseline leg are the only callers.  The HIP library never
+imports this module, and this module never imports the HIP library.
+
+All functions take and return numpy arrays.  Weights are float64 (N, d);
+data is float32 (n, d) and widened exactly inside the C code.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "som_oracle.c")
+_LIB = os.path.join(_HERE, "libsom_oracle.so")
+
+RECT, HEX = 0, 1
+LINEAR, EXPONENTIAL = 0, 1
+
+
+class Schedule(C.Structure):
+    _fields_ = [("lr0", C.c_double), ("lr1", C.c_double),
+                ("lr_decay", C.c_int32),
+                ("sigma0", C.c_double), ("sigma1", C.c_double),
+                ("sigma_decay", C.c_int32)]
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (plain -O2, no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB):
+        cmd = ["gcc", "-O2", "-std=gnu11", "-fopenmp", "-ffp-contract=off",
+               "-fno-fast-math", "-shared", "-fPIC", "-Wall", "-Wextra",
+               "-o", _LIB + ".tmp", _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        L = C.CDLL(_LIB)
+        dp = C.POINTER(C.c_double)
+        fp = C.POINTER(C.c_float)
+        ip = C.POINTER(C.c_int32)
+        up = C.POINTER(C.c_uint64)
+        L.som_oracle_splitmix64.argtypes = [C.c_uint64, C.c_int64, up]
+        L.som_oracle_init_uniform.argtypes = [C.c_uint64, C.c_int64, dp]
+        L.som_oracle_shuffle.argtypes = [C.c_uint64, C.c_int64, C.c_int64, ip]
+        L.som_oracle_schedule_at.argtypes = [C.c_int64, C.c_int64,
+                                             C.POINTER(Schedule), dp, dp]
+        L.som_oracle_position.argtypes = [C.c_int32, C.c_int32, C.c_int64, dp, dp]
+        L.som_oracle_neighbourhood.argtypes = [C.c_int32, C.c_int32, C.c_int32,
+                                               C.c_int64, C.c_double, C.c_double, dp]
+        L.som_oracle_distances.argtypes = [dp, C.c_int64, C.c_int64, fp, dp]
+        L.som_oracle_train.argtypes = [dp, C.c_int32, C.c_int32, C.c_int32,
+                                       C.c_int64, fp, C.c_int64, ip, C.c_int64,
+                                       C.c_int64, C.c_int64, C.POINTER(Schedule),
+                                       ip, C.c_int]
+        L.som_oracle_train.restype = C.c_int
+        L.som_oracle_evaluate.argtypes = [dp, C.c_int32, C.c_int32, C.c_int32,
+                                          C.c_int64, fp, C.c_int64, ip, ip, dp,
+                                          dp, dp, dp, C.c_int]
+        L.som_oracle_evaluate.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a, ct):
+    return a.ctypes.data_as(C.POINTER(ct))
+
+
+def default_threads() -> int:
+    try:
+        return max(1, len(os.sched_getaffinity(0)))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def schedule(lr0, lr1, sigma0, sigma1, lr_decay=LINEAR,
+             sigma_decay=EXPONENTIAL) -> Schedule:
+    return Schedule(float(lr0), float(lr1), int(lr_decay), float(sigma0),
+                    float(sigma1), int(sigma_decay))
+
+
+def splitmix64(seed: int, count: int) -> np.ndarray:
+    out = np.empty(count, dtype=np.uint64)
+    lib().som_oracle_splitmix64(C.c_uint64(seed), count, _p(out, C.c_uint64))
+    return out
+
+
+def init_uniform(seed: int, N: int, d: int) -> np.ndarray:
+    """Initial prototypes U[0,1) on the 2^-24 grid, (N, d) float64."""
+    out = np.empty((N, d), dtype=np.float64)
+    lib().som_oracle_init_uniform(C.c_uint64(seed), N * d, _p(out, C.c_double))
+    return out
+
+
+def shuffle(seed: int, epoch: int, n: int) -> np.ndarray:
+    out = np.empty(n, dtype=np.int32)
+    lib().som_oracle_shuffle(C.c_uint64(seed), epoch, n, _p(out, C.c_int32))
+    return out
+
+
+def schedule_at(t: int, T: int, s: Schedule):
+    lr = C.c_double()
+    sg = C.c_double()
+    lib().som_oracle_schedule_at(t, T, C.byref(s), C.byref(lr), C.byref(sg))
+    return lr.value, sg.value
+
+
+def position(topology: int, cols: int, u: int):
+    y = C.c_double()
+    x = C.c_double()
+    lib().som_oracle_position(topology, cols, u, C.byref(y), C.byref(x))
+    return y.value, x.value
+
+
+def neighbourhood(rows, cols, topology, c, lr, sigma) -> np.ndarray:
+    h = np.empty(rows * cols, dtype=np.float64)
+    lib().som_oracle_neighbourhood(rows, cols, topology, c, float(lr),
+                                   float(sigma), _p(h, C.c_double))
+    return h
+
+
+def distances(W: np.ndarray, x: np.ndarray) -> np.ndarray:
+    W = np.ascontiguousarray(W, dtype=np.float64)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    N, d = W.shape
+    D = np.empty(N, dtype=np.float64)
+    lib().som_oracle_distances(_p(W, C.c_double), N, d, _p(x, C.c_float),
+                               _p(D, C.c_double))
+    return D
+
+
+def train(W: np.ndarray, rows: int, cols: int, X: np.ndarray,
+          order: np.ndarray, s: Schedule, step0: int = 0,
+          total_steps: Optional[int] = None, topology: int = RECT,
+          nthreads: Optional[int] = None, trace: bool = False):
+    """Run len(order) online steps on a float64 copy of W; returns (W, trace)."""
+    W = np.array(W, dtype=np.float64, order="C", copy=True)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    order = np.ascontiguousarray(order, dtype=np.int32)
+    n, d = X.shape
+    assert W.shape == (rows * cols, d)
+    nsteps = order.shape[0]
+    T = step0 + nsteps if total_steps is None else int(total_steps)
+    tr = np.full(nsteps, -1, dtype=np.int32) if trace else None
+    rc = lib().som_oracle_train(
+        _p(W, C.c_double), rows, cols, topology, d, _p(X, C.c_float), n,
+        _p(order, C.c_int32), nsteps, step0, T, C.byref(s),
+        _p(tr, C.c_int32) if trace else None,
+        default_threads() if nthreads is None else nthreads)
+    if rc != 0:
+        raise ValueError(f"som_oracle_train: bad arguments (rc={rc})")
+    return W, tr
+
+
+def evaluate(W: np.ndarray, rows: int, cols: int, X: np.ndarray,
+             topology: int = RECT, nthreads: Optional[int] = None) -> dict:
+    """First/second BMU, squared distances, QE and TE of every sample."""
+    W = np.ascontiguousarray(W, dtype=np.float64)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    n, d = X.shape
+    c1 = np.empty(n, dtype=np.int32)
+    c2 = np.empty(n, dtype=np.int32)
+    d1 = np.empty(n, dtype=np.float64)
+    d2 = np.empty(n, dtype=np.float64)
+    qe = C.c_double()
+    te = C.c_double()
+    rc = lib().som_oracle_evaluate(
+        _p(W, C.c_double), rows, cols, topology, d, _p(X, C.c_float), n,
+        _p(c1, C.c_int32), _p(c2, C.c_int32), _p(d1, C.c_double),
+        _p(d2, C.c_double), C.byref(qe), C.byref(te),
+        default_threads() if nthreads is None else nthreads)
+    if rc != 0:
+        raise ValueError(f"som_oracle_evaluate: bad arguments (rc={rc})")
+    return {"c1": c1, "c2": c2, "d1": d1, "d2": d2, "qe": qe.value,
+            "te": te.value}
