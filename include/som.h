@@ -1,0 +1,192 @@
+/*
+ * som.h -- C ABI of libsom, an MI355X (gfx950) library for online
+ * self-organizing-map (SOM) training on high-dimensional document vectors.
+ *
+ * The method (paper Sec. 5A, Eq. (1); GPU procedure Sec. 6C): a map of
+ * rows x cols units, each with a prototype w_u of length d, is trained one
+ * sample x at a time.  Every step computes the squared Euclidean distance of x
+ * to every prototype, takes the best-matching unit (BMU) c as the arg-min
+ * (lowest index among equal minima), and moves every prototype toward x:
+ *
+ *     w_u <- w_u + h_u (x - w_u),  h_u = lr(t) exp(-|pos(u) - pos(c)|^2 / (2 sigma(t)^2))
+ *
+ * while the learning rate lr and the neighbourhood radius sigma decay over
+ * the steps (Sec. 6D).  The trained map then assigns each document to its BMU
+ * (Sec. 8A) and is scored by its quantization error (Sec. 6D, Sec. 8B).
+ *
+ * Conventions shared by every call:
+ *   - Every call returns a som_status.  No call throws or aborts.
+ *   - Arguments are validated before any device work; a call that returns
+ *     SOM_E_ARG has enqueued nothing and changed nothing.
+ *   - Data pointers named "device" must point into device memory (hipMalloc
+ *     or a torch CUDA tensor) that covers the stated extent; the library
+ *     checks both and returns SOM_E_ARG otherwise.  They stay owned by the
+ *     caller and must stay valid until the map's stream reaches the end of
+ *     the call.
+ *   - Calls are ordered on the map's stream (som_set_stream) and return
+ *     after enqueueing, except where a call says it synchronizes.  A device
+ *     error inside an asynchronous call (for example a bad sample index in a
+ *     caller-supplied order, or a training kernel whose grid barrier timed
+ *     out) is reported by the next synchronizing call on that map.
+ *   - A map is not thread-safe: use one map per host thread.
+ *   - Floating point: prototypes and data are fp32; distances are fp32 sums;
+ *     the schedule and the neighbourhood factors are evaluated in fp64 and
+ *     rounded once to fp32; QE and TE are accumulated in fp64.
+ */
+#ifndef SOM_H
+#define SOM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum som_status {
+    SOM_OK = 0,
+    SOM_E_ARG = 1,         /* invalid argument; nothing was done            */
+    SOM_E_OOM = 2,         /* device allocation failed or over the cap      */
+    SOM_E_DEVICE = 3,      /* HIP runtime error                             */
+    SOM_E_LAUNCH = 4,      /* the cooperative grid cannot be co-resident    */
+    SOM_E_TIMEOUT = 5,     /* a grid barrier did not complete in time       */
+    SOM_E_UNSUPPORTED = 6, /* shape outside what the kernels are built for  */
+    SOM_E_BAD_ORDER = 7    /* a caller-supplied sample index was outside [0, n) */
+} som_status;
+
+/* Lattice of the map.  RECT: unit u = r * cols + c sits at (r, c).  HEX
+ * (the paper's choice, Sec. 6C): odd rows shifted by half a unit, rows
+ * sqrt(3)/2 apart.  Lattice distance is Euclidean, without wrap-around. */
+typedef enum som_topology { SOM_RECT = 0, SOM_HEX = 1 } som_topology;
+
+/* Decay law of lr and sigma between their endpoint values a (step 0) and b
+ * (step T-1), at p = t / (T - 1) (p = 0 when T = 1):
+ *   LINEAR       (1 - p) a + p b
+ *   EXPONENTIAL  a^(1-p) b^p            (needs a > 0 and b > 0)
+ * Equal endpoints give that constant value (also +inf for sigma). */
+typedef enum som_decay { SOM_DECAY_LINEAR = 0, SOM_DECAY_EXPONENTIAL = 1 } som_decay;
+
+/* Training schedule (paper Sec. 6D: lr and the neighbourhood radius decay).
+ *   lr0, lr1        learning rate at the first and last step; >= 0, finite.
+ *   sigma0, sigma1  radius at the first and last step; >= 0 (+inf allowed for
+ *                   a constant radius).  sigma = 0 makes h a Kronecker delta
+ *                   at the BMU; sigma = +inf makes h = lr for every unit.
+ *   shuffle_seed    used only when order == NULL: epoch e presents the
+ *                   samples in a Fisher-Yates permutation drawn from the
+ *                   e-th SplitMix64 output of shuffle_seed (see som_shuffle).
+ *   order           NULL, or a device int32 array of epochs * n sample
+ *                   indices, entry k being the sample of the call's step k.
+ *   step0           global index of the call's first step (to resume).
+ *   total_steps     T, the schedule's length; 0 means step0 + epochs * n.
+ *                   Must be >= step0 + epochs * n.
+ *   bmu_trace       NULL, or a device int32 array of epochs * n entries that
+ *                   receives the BMU of every step.                            */
+typedef struct som_schedule {
+    double lr0;
+    double lr1;
+    int32_t lr_decay;
+    double sigma0;
+    double sigma1;
+    int32_t sigma_decay;
+    uint64_t shuffle_seed;
+    const int32_t *order;
+    int64_t step0;
+    int64_t total_steps;
+    int32_t *bmu_trace;
+} som_schedule;
+
+typedef struct som_map som_map;
+
+/* Create a rows x cols map of d-dimensional fp32 prototypes on the current
+ * HIP device and initialise them U[0,1): element i = u * d + j is the top
+ * 24 bits of the i-th SplitMix64 output of `seed`, times 2^-24 (the paper
+ * initialises on the principal-component plane, Sec. 6D; that is not built
+ * here).  The prototypes are owned by the map.  Topology starts as RECT and
+ * the stream as the null stream.
+ * Errors: SOM_E_ARG (rows, cols or d <= 0, rows * cols > 2^24 - 1,
+ * rows * cols * d overflows, out == NULL), SOM_E_OOM, SOM_E_DEVICE.
+ * Synchronizes the device once (initialisation). */
+som_status som_create(int32_t rows, int32_t cols, int32_t d, uint64_t seed,
+                      som_map **out);
+
+/* Release the map and its device memory after the stream drains.  NULL is
+ * a no-op. */
+som_status som_destroy(som_map *map);
+
+/* SOM_RECT or SOM_HEX; SOM_E_ARG otherwise. */
+som_status som_set_topology(som_map *map, int32_t topology);
+
+/* Order all later calls on `stream` (a hipStream_t, e.g. torch's
+ * torch.cuda.current_stream().cuda_stream); NULL selects the null stream. */
+som_status som_set_stream(som_map *map, void *stream);
+
+/* Online training (paper Sec. 5A and 6C): epochs * n steps over the n x d
+ * row-major fp32 device matrix X, as one persistent cooperative kernel that
+ * keeps the whole per-sample loop on the device.  Stream-ordered.
+ * Errors: SOM_E_ARG (map, X or sched NULL, n <= 0, epochs <= 0, epochs * n
+ * beyond 2^31 - 1, bad decay kind, lr < 0 or not finite, sigma < 0 or NaN,
+ * exponential decay with a zero or infinite endpoint, total_steps too small,
+ * X, order or bmu_trace not covering their extent), SOM_E_UNSUPPORTED
+ * (d above the largest built kernel shape), SOM_E_LAUNCH, SOM_E_DEVICE.
+ * An order entry outside [0, n) stops the kernel before any update and is
+ * reported as SOM_E_BAD_ORDER by the next synchronizing call. */
+som_status som_train(som_map *map, const float *X, int64_t n, int32_t epochs,
+                     const som_schedule *sched);
+
+/* Batched BMU assignment (Sec. 8A): for each of the n rows of the device
+ * matrix X, out_idx[i] = BMU index (lowest index among equal minima).
+ * Candidates are ranked with fp32 matrix-core products
+ * ||w||^2 - 2 x.w and the best few re-ranked by direct fp32 distances.
+ * out_idx is a device int32 array of n entries.  Stream-ordered. */
+som_status som_bmu(som_map *map, const float *X, int64_t n, int32_t *out_idx);
+
+/* As som_bmu, also writing the second BMU (out_idx2, -1 for a one-unit map)
+ * and the squared distance to the BMU (out_d1, fp32).  Any of the three
+ * outputs may be NULL.  Device arrays of n entries.  Stream-ordered. */
+som_status som_bmu2(som_map *map, const float *X, int64_t n, int32_t *out_idx,
+                    int32_t *out_idx2, float *out_d1);
+
+/* Quantization error (Sec. 6D, Sec. 8B): mean over the n samples of the
+ * unsquared Euclidean distance to the BMU, accumulated in fp64.  *out_qe is
+ * a host double.  Synchronizes the stream. */
+som_status som_quantization_error(som_map *map, const float *X, int64_t n,
+                                  double *out_qe);
+
+/* Topographic error: fraction of the n samples whose first and second BMUs
+ * are not lattice neighbours (lattice distance > 1); 0 for a one-unit map.
+ * *out_te is a host double.  Synchronizes the stream. */
+som_status som_topographic_error(som_map *map, const float *X, int64_t n,
+                                 double *out_te);
+
+/* Copy the rows*cols x d prototypes (row-major, unit u = r * cols + c) out
+ * to / in from `dst` / `src`, a host or device pointer of rows*cols*d floats.
+ * Used to start from a given state and to checkpoint and resume.
+ * Synchronize the stream. */
+som_status som_get_weights(som_map *map, float *dst);
+som_status som_set_weights(som_map *map, const float *src);
+
+/* Wait for the map's stream and report any deferred device error. */
+som_status som_synchronize(som_map *map);
+
+/* rows, cols, d and topology of a map; any output may be NULL. */
+som_status som_get_shape(const som_map *map, int32_t *rows, int32_t *cols,
+                         int32_t *d, int32_t *topology);
+
+/* The Fisher-Yates permutation of [0, n) that som_train uses for epoch
+ * `epoch` when no order is given (host int32 array of n entries). */
+som_status som_shuffle(uint64_t seed, int64_t epoch, int64_t n, int32_t *out);
+
+/* Launch shape that som_train would use for this map: workgroups, threads
+ * per workgroup and kernel variant (0 = prototypes streamed from memory each
+ * step, 1 = prototypes held in LDS for the whole call).  Any output may be
+ * NULL. */
+som_status som_train_plan(const som_map *map, int32_t *grid, int32_t *block,
+                          int32_t *variant);
+
+/* Human-readable name of a status code (static storage). */
+const char *som_status_string(som_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOM_H */

@@ -1,0 +1,480 @@
+// Host runtime of libsom: the C ABI declared in include/som.h.
+//
+// Owns the map (prototypes in device memory, row pitch padded to a multiple
+// of 4 floats so rows can be read as 16-byte vectors), validates every
+// argument before any device work, builds the per-epoch sample order when
+// the caller gives none, and launches the kernels on the map's stream.
+#include "som.h"
+#include "som_internal.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+struct som_map {
+    int32_t rows = 0, cols = 0, d = 0, topology = SOM_RECT;
+    int32_t N = 0;
+    int64_t ld = 0;  // row pitch in floats
+    int device = 0;
+    int num_cus = 0;
+    hipStream_t stream = nullptr;
+    float *W = nullptr;
+    som::DevState *state = nullptr;
+    unsigned long long *slots = nullptr;
+    int32_t nslots = 0;
+    // order staging for library-shuffled training
+    int32_t *order_dev = nullptr;
+    int64_t order_cap = 0;
+    int32_t *order_host = nullptr;  // pinned
+    hipEvent_t order_done = nullptr;
+    // evaluation scratch
+    float *wnorm = nullptr;
+    int32_t *cand = nullptr, *idx1 = nullptr, *idx2 = nullptr;
+    float *d1 = nullptr;
+    double *sums = nullptr;
+    int64_t eval_cap = 0;
+};
+
+namespace {
+
+constexpr uint64_t kMaxBytesDefault = 64ull << 30;  // per-map device memory cap
+
+uint64_t max_bytes() {
+    const char *e = getenv("SOM_MAX_BYTES");
+    if (e && *e) {
+        char *end = nullptr;
+        unsigned long long v = strtoull(e, &end, 10);
+        if (end && *end == '\0' && v > 0) return v;
+    }
+    return kMaxBytesDefault;
+}
+
+som_status from_hip(hipError_t e) {
+    if (e == hipSuccess) return SOM_OK;
+    if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation) return SOM_E_OOM;
+    if (e == hipErrorCooperativeLaunchTooLarge) return SOM_E_LAUNCH;
+    return SOM_E_DEVICE;
+}
+
+// True when [p, p + bytes) lies inside one device allocation.
+bool device_range_ok(const void *p, uint64_t bytes) {
+    if (!p) return false;
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged) return false;
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, const_cast<void *>(p)) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    const uintptr_t b = reinterpret_cast<uintptr_t>(base);
+    const uintptr_t q = reinterpret_cast<uintptr_t>(p);
+    return q >= b && bytes <= size && q - b <= size - bytes;
+}
+
+bool schedule_ok(const som_schedule *s) {
+    if (s->lr_decay != SOM_DECAY_LINEAR && s->lr_decay != SOM_DECAY_EXPONENTIAL) return false;
+    if (s->sigma_decay != SOM_DECAY_LINEAR && s->sigma_decay != SOM_DECAY_EXPONENTIAL)
+        return false;
+    if (!(s->lr0 >= 0.0) || !(s->lr1 >= 0.0) || isinf(s->lr0) || isinf(s->lr1)) return false;
+    if (!(s->sigma0 >= 0.0) || !(s->sigma1 >= 0.0)) return false;  // rejects NaN
+    if (s->lr_decay == SOM_DECAY_EXPONENTIAL && s->lr0 != s->lr1 &&
+        (s->lr0 == 0.0 || s->lr1 == 0.0))
+        return false;
+    if (s->sigma_decay == SOM_DECAY_EXPONENTIAL && s->sigma0 != s->sigma1 &&
+        (s->sigma0 == 0.0 || s->sigma1 == 0.0 || isinf(s->sigma0) || isinf(s->sigma1)))
+        return false;
+    if (s->sigma_decay == SOM_DECAY_LINEAR && s->sigma0 != s->sigma1 &&
+        (isinf(s->sigma0) || isinf(s->sigma1)))
+        return false;
+    return true;
+}
+
+uint64_t splitmix64_at(uint64_t seed, uint64_t i) {
+    uint64_t z = seed + (i + 1u) * 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+void fisher_yates(uint64_t seed, int64_t epoch, int64_t n, int32_t *out) {
+    const uint64_t es = splitmix64_at(seed, (uint64_t)epoch);
+    for (int64_t i = 0; i < n; ++i) out[i] = (int32_t)i;
+    uint64_t k = 0;
+    for (int64_t j = n - 1; j >= 1; --j, ++k) {
+        const uint64_t r = splitmix64_at(es, k);
+        const uint64_t pick = (uint64_t)(((unsigned __int128)r * (uint64_t)(j + 1)) >> 64);
+        const int32_t t = out[j];
+        out[j] = out[pick];
+        out[pick] = t;
+    }
+}
+
+template <typename T>
+som_status grow(T **p, int64_t *cap_bytes_unused, int64_t count) {
+    (void)cap_bytes_unused;
+    if (*p) {
+        hipError_t e = hipFree(*p);
+        *p = nullptr;
+        if (e != hipSuccess) return from_hip(e);
+    }
+    return from_hip(hipMalloc(reinterpret_cast<void **>(p), (size_t)count * sizeof(T)));
+}
+
+som_status ensure_eval_scratch(som_map *m, int64_t n) {
+    if (n <= m->eval_cap) return SOM_OK;
+    hipError_t e = hipStreamSynchronize(m->stream);
+    if (e != hipSuccess) return from_hip(e);
+    som_status st;
+    if ((st = grow(&m->cand, nullptr, n * som::kCand)) != SOM_OK) return st;
+    if ((st = grow(&m->idx1, nullptr, n)) != SOM_OK) return st;
+    if ((st = grow(&m->idx2, nullptr, n)) != SOM_OK) return st;
+    if ((st = grow(&m->d1, nullptr, n)) != SOM_OK) return st;
+    m->eval_cap = n;
+    return SOM_OK;
+}
+
+som_status check_deferred(som_map *m) {
+    som::DevState st;
+    hipError_t e = hipMemcpy(&st, m->state, sizeof(st), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return from_hip(e);
+    if (st.status != 0) {
+        const int32_t zero = 0;
+        e = hipMemcpy(&m->state->status, &zero, sizeof(zero), hipMemcpyHostToDevice);
+        if (e != hipSuccess) return from_hip(e);
+        return (som_status)st.status;
+    }
+    return SOM_OK;
+}
+
+som_status run_eval(som_map *m, const float *X, int64_t n, int32_t *idx1,
+                    int32_t *idx2, float *d1) {
+    som_status st = ensure_eval_scratch(m, n);
+    if (st != SOM_OK) return st;
+    som::EvalArgs a{};
+    a.W = m->W;
+    a.ld = m->ld;
+    a.N = m->N;
+    a.d = m->d;
+    a.rows = m->rows;
+    a.cols = m->cols;
+    a.topology = m->topology;
+    a.X = X;
+    a.n = n;
+    a.wnorm = m->wnorm;
+    a.cand = m->cand;
+    a.idx1 = idx1;
+    a.idx2 = idx2;
+    a.d1 = d1;
+    a.x_vec4 = (m->d % 4 == 0) && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
+    hipError_t e = som::launch_row_sqnorm(m->W, m->ld, m->N, m->wnorm, m->stream);
+    if (e == hipSuccess) e = som::launch_bmu_candidates(a, m->stream);
+    if (e == hipSuccess) e = som::launch_bmu_rerank(a, m->stream);
+    return from_hip(e);
+}
+
+bool eval_args_ok(som_map *m, const float *X, int64_t n) {
+    if (!m || !X || n <= 0 || n > INT32_MAX) return false;
+    return device_range_ok(X, (uint64_t)n * (uint64_t)m->d * sizeof(float));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *som_status_string(som_status s) {
+    switch (s) {
+        case SOM_OK: return "ok";
+        case SOM_E_ARG: return "invalid argument";
+        case SOM_E_OOM: return "out of device memory";
+        case SOM_E_DEVICE: return "device error";
+        case SOM_E_LAUNCH: return "cooperative grid cannot be co-resident";
+        case SOM_E_TIMEOUT: return "grid barrier timed out";
+        case SOM_E_UNSUPPORTED: return "shape not supported by the built kernels";
+        case SOM_E_BAD_ORDER: return "sample order holds an index outside [0, n)";
+    }
+    return "unknown status";
+}
+
+som_status som_shuffle(uint64_t seed, int64_t epoch, int64_t n, int32_t *out) {
+    if (!out || n <= 0 || n > INT32_MAX || epoch < 0) return SOM_E_ARG;
+    fisher_yates(seed, epoch, n, out);
+    return SOM_OK;
+}
+
+som_status som_create(int32_t rows, int32_t cols, int32_t d, uint64_t seed,
+                      som_map **out) {
+    if (!out || rows <= 0 || cols <= 0 || d <= 0) return SOM_E_ARG;
+    *out = nullptr;
+    const int64_t N = (int64_t)rows * cols;
+    if (N > som::kMaxUnits) return SOM_E_ARG;
+    const int64_t ld = ((int64_t)d + 3) / 4 * 4;
+    const uint64_t bytes = (uint64_t)N * (uint64_t)ld * sizeof(float);
+    if (bytes / sizeof(float) / (uint64_t)ld != (uint64_t)N) return SOM_E_ARG;
+    if (bytes > max_bytes()) return SOM_E_OOM;
+
+    som_map *m = new (std::nothrow) som_map();
+    if (!m) return SOM_E_OOM;
+    m->rows = rows;
+    m->cols = cols;
+    m->d = d;
+    m->N = (int32_t)N;
+    m->ld = ld;
+    hipError_t e = hipGetDevice(&m->device);
+    if (e == hipSuccess)
+        e = hipDeviceGetAttribute(&m->num_cus, hipDeviceAttributeMultiprocessorCount,
+                                  m->device);
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->W), bytes);
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->state), sizeof(som::DevState));
+    if (e == hipSuccess) e = hipMemset(m->state, 0, sizeof(som::DevState));
+    if (e == hipSuccess) {
+        m->nslots = 2 * (m->num_cus > 0 ? m->num_cus : 1);
+        if (m->nslots < 2 * 1024) m->nslots = 2 * 1024;
+        e = hipMalloc(reinterpret_cast<void **>(&m->slots),
+                      (size_t)m->nslots * sizeof(unsigned long long));
+    }
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->wnorm), (size_t)N * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->sums), 2 * sizeof(double));
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&m->order_done, hipEventDisableTiming);
+    if (e == hipSuccess) e = som::launch_init_uniform(m->W, ld, m->N, d, seed, nullptr);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        som_destroy(m);
+        return from_hip(e);
+    }
+    *out = m;
+    return SOM_OK;
+}
+
+som_status som_destroy(som_map *m) {
+    if (!m) return SOM_OK;
+    if (m->stream) (void)hipStreamSynchronize(m->stream);
+    else (void)hipDeviceSynchronize();
+    (void)hipFree(m->W);
+    (void)hipFree(m->state);
+    (void)hipFree(m->slots);
+    (void)hipFree(m->order_dev);
+    if (m->order_host) (void)hipHostFree(m->order_host);
+    if (m->order_done) (void)hipEventDestroy(m->order_done);
+    (void)hipFree(m->wnorm);
+    (void)hipFree(m->cand);
+    (void)hipFree(m->idx1);
+    (void)hipFree(m->idx2);
+    (void)hipFree(m->d1);
+    (void)hipFree(m->sums);
+    delete m;
+    return SOM_OK;
+}
+
+som_status som_set_topology(som_map *m, int32_t topology) {
+    if (!m || (topology != SOM_RECT && topology != SOM_HEX)) return SOM_E_ARG;
+    m->topology = topology;
+    return SOM_OK;
+}
+
+som_status som_set_stream(som_map *m, void *stream) {
+    if (!m) return SOM_E_ARG;
+    m->stream = reinterpret_cast<hipStream_t>(stream);
+    return SOM_OK;
+}
+
+som_status som_get_shape(const som_map *m, int32_t *rows, int32_t *cols, int32_t *d,
+                         int32_t *topology) {
+    if (!m) return SOM_E_ARG;
+    if (rows) *rows = m->rows;
+    if (cols) *cols = m->cols;
+    if (d) *d = m->d;
+    if (topology) *topology = m->topology;
+    return SOM_OK;
+}
+
+static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
+    som::TrainArgs a{};
+    a.W = m->W;
+    a.ld = m->ld;
+    a.N = m->N;
+    a.d = m->d;
+    a.rows = m->rows;
+    a.cols = m->cols;
+    a.topology = m->topology;
+    a.X = X;
+    a.n = n;
+    a.slots = m->slots;
+    a.state = m->state;
+    a.x_vec4 = (m->d % 4 == 0) && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
+    const char *g = getenv("SOM_TRAIN_GRID");
+    a.grid = (g && *g) ? atoi(g) : 0;
+    if (a.grid > m->nslots / 2) a.grid = m->nslots / 2;
+    a.timeout_ticks = 100000000ull * 20;  // 20 s at the 100 MHz reference clock
+    return a;
+}
+
+som_status som_train_plan(const som_map *m, int32_t *grid, int32_t *block,
+                          int32_t *variant) {
+    if (!m) return SOM_E_ARG;
+    som::TrainArgs a = train_args(const_cast<som_map *>(m), nullptr, 1);
+    som::TrainPlan p;
+    hipError_t e = som::plan_train(a, m->num_cus, &p);
+    if (e == hipErrorInvalidValue) return SOM_E_UNSUPPORTED;
+    if (e != hipSuccess) return from_hip(e);
+    if (grid) *grid = p.grid;
+    if (block) *block = p.block;
+    if (variant) *variant = p.variant;
+    return SOM_OK;
+}
+
+som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
+                     const som_schedule *s) {
+    if (!m || !X || !s || n <= 0 || epochs <= 0) return SOM_E_ARG;
+    if (n > INT32_MAX || (int64_t)epochs * n > INT32_MAX) return SOM_E_ARG;
+    if (!schedule_ok(s)) return SOM_E_ARG;
+    const int64_t nsteps = (int64_t)epochs * n;
+    if (s->step0 < 0) return SOM_E_ARG;
+    const int64_t total = s->total_steps == 0 ? s->step0 + nsteps : s->total_steps;
+    if (total < s->step0 + nsteps) return SOM_E_ARG;
+    if (!device_range_ok(X, (uint64_t)n * (uint64_t)m->d * sizeof(float))) return SOM_E_ARG;
+    if (s->order && !device_range_ok(s->order, (uint64_t)nsteps * sizeof(int32_t)))
+        return SOM_E_ARG;
+    if (s->bmu_trace && !device_range_ok(s->bmu_trace, (uint64_t)nsteps * sizeof(int32_t)))
+        return SOM_E_ARG;
+
+    som::TrainArgs a = train_args(m, X, n);
+    som::TrainPlan plan;
+    hipError_t e = som::plan_train(a, m->num_cus, &plan);
+    if (e == hipErrorInvalidValue) return SOM_E_UNSUPPORTED;
+    if (e != hipSuccess) return from_hip(e);
+
+    const int32_t *order = s->order;
+    if (!order) {
+        // Library order: epoch e = t / n presents permutation e of [0, n).
+        if (m->order_cap < nsteps) {
+            e = hipStreamSynchronize(m->stream);
+            if (e == hipSuccess && m->order_dev) e = hipFree(m->order_dev);
+            m->order_dev = nullptr;
+            if (e == hipSuccess && m->order_host) e = hipHostFree(m->order_host);
+            m->order_host = nullptr;
+            m->order_cap = 0;
+            if (e == hipSuccess)
+                e = hipMalloc(reinterpret_cast<void **>(&m->order_dev), (size_t)nsteps * 4);
+            if (e == hipSuccess)
+                e = hipHostMalloc(reinterpret_cast<void **>(&m->order_host), (size_t)nsteps * 4,
+                                  hipHostMallocDefault);
+            if (e != hipSuccess) return from_hip(e);
+            m->order_cap = nsteps;
+        }
+        e = hipEventSynchronize(m->order_done);  // previous upload has left the buffer
+        if (e != hipSuccess) return from_hip(e);
+        std::vector<int32_t> perm((size_t)n);
+        int64_t cur_epoch = -1;
+        for (int64_t k = 0; k < nsteps; ++k) {
+            const int64_t t = s->step0 + k;
+            const int64_t ep = t / n;
+            if (ep != cur_epoch) {
+                fisher_yates(s->shuffle_seed, ep, n, perm.data());
+                cur_epoch = ep;
+            }
+            m->order_host[k] = perm[(size_t)(t % n)];
+        }
+        e = hipMemcpyAsync(m->order_dev, m->order_host, (size_t)nsteps * 4,
+                           hipMemcpyHostToDevice, m->stream);
+        if (e == hipSuccess) e = hipEventRecord(m->order_done, m->stream);
+        if (e != hipSuccess) return from_hip(e);
+        order = m->order_dev;
+    }
+
+    a.order = order;
+    a.nsteps = nsteps;
+    a.step0 = s->step0;
+    a.total_steps = total;
+    a.lr0 = s->lr0;
+    a.lr1 = s->lr1;
+    a.sigma0 = s->sigma0;
+    a.sigma1 = s->sigma1;
+    a.lr_decay = s->lr_decay;
+    a.sigma_decay = s->sigma_decay;
+    a.bmu_trace = s->bmu_trace;
+    e = som::launch_prepare_train(order, nsteps, n, m->slots, m->nslots, m->state, m->stream);
+    if (e == hipSuccess) e = som::launch_train(a, plan, m->stream);
+    return from_hip(e);
+}
+
+som_status som_bmu2(som_map *m, const float *X, int64_t n, int32_t *out_idx,
+                    int32_t *out_idx2, float *out_d1) {
+    if (!eval_args_ok(m, X, n)) return SOM_E_ARG;
+    if (out_idx && !device_range_ok(out_idx, (uint64_t)n * 4)) return SOM_E_ARG;
+    if (out_idx2 && !device_range_ok(out_idx2, (uint64_t)n * 4)) return SOM_E_ARG;
+    if (out_d1 && !device_range_ok(out_d1, (uint64_t)n * 4)) return SOM_E_ARG;
+    som_status st = ensure_eval_scratch(m, n);
+    if (st != SOM_OK) return st;
+    return run_eval(m, X, n, out_idx ? out_idx : m->idx1, out_idx2, out_d1);
+}
+
+som_status som_bmu(som_map *m, const float *X, int64_t n, int32_t *out_idx) {
+    if (!out_idx) return SOM_E_ARG;
+    return som_bmu2(m, X, n, out_idx, nullptr, nullptr);
+}
+
+static som_status qe_te(som_map *m, const float *X, int64_t n, double *qe, double *te) {
+    if (!eval_args_ok(m, X, n)) return SOM_E_ARG;
+    som_status st = ensure_eval_scratch(m, n);
+    if (st != SOM_OK) return st;
+    st = run_eval(m, X, n, m->idx1, m->idx2, m->d1);
+    if (st != SOM_OK) return st;
+    hipError_t e = som::launch_qe_te_reduce(m->idx1, m->idx2, m->d1, n, m->cols,
+                                            m->topology, m->sums, m->stream);
+    double h[2] = {0.0, 0.0};
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(h, m->sums, sizeof(h), hipMemcpyDeviceToHost, m->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+    if (e != hipSuccess) return from_hip(e);
+    st = check_deferred(m);
+    if (st != SOM_OK) return st;
+    if (qe) *qe = h[0] / (double)n;
+    if (te) *te = h[1] / (double)n;
+    return SOM_OK;
+}
+
+som_status som_quantization_error(som_map *m, const float *X, int64_t n, double *out_qe) {
+    if (!out_qe) return SOM_E_ARG;
+    return qe_te(m, X, n, out_qe, nullptr);
+}
+
+som_status som_topographic_error(som_map *m, const float *X, int64_t n, double *out_te) {
+    if (!out_te) return SOM_E_ARG;
+    return qe_te(m, X, n, nullptr, out_te);
+}
+
+som_status som_get_weights(som_map *m, float *dst) {
+    if (!m || !dst) return SOM_E_ARG;
+    hipError_t e = hipMemcpy2DAsync(dst, (size_t)m->d * 4, m->W, (size_t)m->ld * 4,
+                                    (size_t)m->d * 4, (size_t)m->N, hipMemcpyDefault,
+                                    m->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+    if (e != hipSuccess) return from_hip(e);
+    return check_deferred(m);
+}
+
+som_status som_set_weights(som_map *m, const float *src) {
+    if (!m || !src) return SOM_E_ARG;
+    hipError_t e = hipMemcpy2DAsync(m->W, (size_t)m->ld * 4, src, (size_t)m->d * 4,
+                                    (size_t)m->d * 4, (size_t)m->N, hipMemcpyDefault,
+                                    m->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+    if (e != hipSuccess) return from_hip(e);
+    return check_deferred(m);
+}
+
+som_status som_synchronize(som_map *m) {
+    if (!m) return SOM_E_ARG;
+    hipError_t e = hipStreamSynchronize(m->stream);
+    if (e != hipSuccess) return from_hip(e);
+    return check_deferred(m);
+}
+
+}  // extern "C"

@@ -1,0 +1,99 @@
+// Internal declarations shared by the host runtime (som_api.cpp) and the
+// kernel translation units.  Not part of the public ABI (include/som.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace som {
+
+// Threads per workgroup of the persistent training kernel.
+constexpr int kTrainBlock = 256;
+// Grid-exchange slot layout: 64-bit key = dist_bits << 32 | tag << 24 | unit.
+constexpr int kUnitBits = 24;
+constexpr int32_t kMaxUnits = (1 << kUnitBits) - 1;
+
+// Device-side status words of a map (one allocation, zeroed at creation).
+struct DevState {
+    int32_t status;     // sticky error code (som_status), cleared by the host
+    int32_t order_bad;  // 1 if the current call's order has an index outside [0, n)
+    int32_t pad[2];
+};
+
+struct TrainArgs {
+    float *W;               // N x ld, row-major, ld % 4 == 0, zero padding
+    int64_t ld;             // row pitch in floats
+    int32_t N, d, rows, cols, topology;
+    const float *X;         // n x d, row-major
+    int64_t n;
+    const int32_t *order;   // nsteps sample indices
+    int64_t nsteps, step0, total_steps;
+    double lr0, lr1, sigma0, sigma1;
+    int32_t lr_decay, sigma_decay;
+    int32_t *bmu_trace;     // nullable, nsteps entries
+    unsigned long long *slots;  // 2 * grid exchange slots
+    DevState *state;
+    int32_t grid;
+    int32_t x_vec4;         // X rows may be read as float4 (d % 4 == 0, aligned)
+    uint64_t timeout_ticks; // bound of one exchange wait, in 100 MHz ticks
+};
+
+struct TrainPlan {
+    int32_t grid = 0;
+    int32_t block = kTrainBlock;
+    int32_t variant = 0;     // 0 = streamed prototypes
+    int32_t kslots = 0;      // float4 columns per lane (template instance)
+    size_t lds_bytes = 0;
+};
+
+// Squared lattice distance between units u and c of a map with `cols`
+// columns.  RECT: unit r * cols + c sits at (r, c).  HEX: odd rows are
+// shifted by half a unit and rows are sqrt(3)/2 apart.  No wrap-around.
+__device__ inline double lattice_sq(int u, int c, int cols, int topology) {
+    const int ru = u / cols, cu = u - ru * cols;
+    const int rc = c / cols, cc = c - rc * cols;
+    if (topology == 1) {
+        const double pitch = 0.86602540378443864676;  // sqrt(3) / 2
+        const double xu = cu + ((ru & 1) ? 0.5 : 0.0), xc = cc + ((rc & 1) ? 0.5 : 0.0);
+        const double yu = ru * pitch, yc = rc * pitch;
+        return (yu - yc) * (yu - yc) + (xu - xc) * (xu - xc);
+    }
+    const double dr = ru - rc, dc = cu - cc;
+    return dr * dr + dc * dc;
+}
+
+// Host-side launchers (each translation unit owns its kernels).
+hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan);
+hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s);
+
+hipError_t launch_init_uniform(float *W, int64_t ld, int32_t N, int32_t d,
+                               uint64_t seed, hipStream_t s);
+hipError_t launch_prepare_train(const int32_t *order, int64_t nsteps, int64_t n,
+                                unsigned long long *slots, int32_t nslots,
+                                DevState *state, hipStream_t s);
+hipError_t launch_row_sqnorm(const float *W, int64_t ld, int32_t N, float *out,
+                             hipStream_t s);
+
+struct EvalArgs {
+    const float *W;
+    int64_t ld;
+    int32_t N, d, rows, cols, topology;
+    const float *X;
+    int64_t n;
+    const float *wnorm;     // N squared prototype norms
+    int32_t *cand;          // n x kCand candidate units (scratch)
+    int32_t *idx1;          // n (required)
+    int32_t *idx2;          // n (nullable)
+    float *d1;              // n (nullable)
+    int32_t x_vec4;
+};
+constexpr int kCand = 4;
+
+hipError_t launch_bmu_candidates(const EvalArgs &a, hipStream_t s);
+hipError_t launch_bmu_rerank(const EvalArgs &a, hipStream_t s);
+// QE and TE sums over n samples from (idx1, idx2, d1); writes 2 doubles.
+hipError_t launch_qe_te_reduce(const int32_t *idx1, const int32_t *idx2,
+                               const float *d1, int64_t n, int32_t cols,
+                               int32_t topology, double *out2, hipStream_t s);
+
+}  // namespace som

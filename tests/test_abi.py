@@ -1,0 +1,79 @@
+"""The C ABI library loads, exports every symbol som.h declares and rejects
+bad arguments on the host before any device work (no GPU needed)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1905_09598_amd as som
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "som.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+char\s*\*|som_status)\s*(som_\w+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = som.lib()
+    names = declared_symbols()
+    assert len(names) >= 14
+    assert set(names) == set(som.EXPORTED)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings():
+    assert som.som_status_string(0) == "ok"
+    for code in range(1, 8):
+        assert som.som_status_string(code) not in ("", "unknown status")
+    assert som.som_status_string(99) == "unknown status"
+
+
+@pytest.mark.parametrize("rows,cols,d", [(0, 3, 4), (3, 0, 4), (3, 3, 0), (-1, 2, 2),
+                                         (4097, 4096, 1)])
+def test_create_rejects_bad_shapes_before_device_work(rows, cols, d):
+    with pytest.raises(som.SomError) as e:
+        som.som_create(rows, cols, d, 0)
+    assert e.value.name == "SOM_E_ARG"
+
+
+def test_create_rejects_null_out_pointer():
+    assert som.lib().som_create(2, 2, 4, C.c_uint64(0), None) == 1
+
+
+def test_calls_on_null_map_are_argument_errors():
+    L = som.lib()
+    s = som.make_schedule(0.5, 0.01, 3.0, 1.0)
+    assert L.som_train(None, None, 10, 1, C.byref(s)) == 1
+    assert L.som_bmu(None, None, 10, None) == 1
+    assert L.som_bmu2(None, None, 10, None, None, None) == 1
+    assert L.som_synchronize(None) == 1
+    assert L.som_set_topology(None, 0) == 1
+    assert L.som_get_weights(None, None) == 1
+    assert L.som_set_weights(None, None) == 1
+    v = C.c_double()
+    assert L.som_quantization_error(None, None, 5, C.byref(v)) == 1
+    assert L.som_topographic_error(None, None, 5, C.byref(v)) == 1
+    assert L.som_destroy(None) == 0
+    assert L.som_get_shape(None, None, None, None, None) == 1
+    assert L.som_train_plan(None, None, None, None) == 1
+
+
+def test_shuffle_argument_errors():
+    with pytest.raises(som.SomError):
+        som.som_shuffle(0, 0, 0)
+    with pytest.raises(som.SomError):
+        som.som_shuffle(0, -1, 5)
+
+
+@pytest.mark.parametrize("seed,epoch,n", [(0, 0, 1), (0, 0, 2), (7, 3, 100), (123, 9, 5000)])
+def test_library_shuffle_matches_independent_oracle_shuffle(seed, epoch, n):
+    lib_perm = som.som_shuffle(seed, epoch, n)
+    assert np.array_equal(lib_perm, oracle.shuffle(seed, epoch, n))
+    assert sorted(lib_perm.tolist()) == list(range(n))

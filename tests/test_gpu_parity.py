@@ -1,0 +1,332 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Criteria (per the workload contract):
+  (1) BMU indices bit-exact on every sample whose oracle top-two relative
+      gap (D2 - D1) / D1 exceeds 1e-4;
+  (2) one training step from identical state: weights within 1e-5 max-abs;
+  (3) after full training, QE and TE within 1 % relative of the oracle's.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1905_09598_amd as som
+import workloads
+from gpu_util import config, dev, golden, oracle_schedule, rel_gap, say, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+GAP = 1e-4
+STEP_ATOL = 1e-5
+
+
+def make_map(rows, cols, d, seed=0, topology=som.RECT, W=None):
+    m = som.Map(rows, cols, d, seed=seed, topology=topology)
+    if W is not None:
+        m.weights = dev(np.asarray(W, dtype=np.float32))
+    return m
+
+
+# ------------------------------------------------------------ initialisation
+@pytest.mark.parametrize("rows,cols,d,seed", [(10, 10, 500, 0), (3, 7, 37, 5),
+                                              (1, 1, 1, 9), (20, 20, 2000, 0)])
+def test_init_matches_oracle_bit_exact(rows, cols, d, seed):
+    say("init", rows, cols, d, seed)
+    m = make_map(rows, cols, d, seed)
+    got = m.weights.cpu().numpy()
+    want = oracle.init_uniform(seed, rows * cols, d).astype(np.float32)
+    assert np.array_equal(got, want)
+    m.close()
+
+
+# ------------------------------------------------------------ batched BMU
+def _bmu_case(rows, cols, d, n, seed, kind="tfidf"):
+    if kind == "tfidf":
+        X = workloads.small_tfidf(n, d, seed)
+        W = workloads.random_weights(rows * cols, d, seed + 1, 0.0, 0.05)
+        # put a few prototypes next to samples so the winners are not all ties
+        k = min(rows * cols, n) // 2
+        W[:k] = 0.7 * X[:k] + 0.3 * W[:k]
+    else:
+        X = workloads.gaussian_mixture(n, d, 8, 0.2, seed)
+        W = workloads.random_weights(rows * cols, d, seed + 1, -1.0, 1.0)
+    return X, W
+
+
+@pytest.mark.parametrize("rows,cols,d,n,kind", [
+    (10, 10, 500, 200, "tfidf"),        # tiny workload's shape
+    (20, 20, 2000, 700, "tfidf"),       # several unit tiles, ragged sample tile
+    (7, 9, 37, 130, "mixture"),         # d not a multiple of 4 or of the k slice
+    (1, 1, 16, 5, "mixture"),           # one-unit map: no second BMU
+    (1, 3, 8, 3, "mixture"),            # fewer units than candidates
+    (30, 30, 5000, 300, "tfidf"),
+    (100, 100, 2048, 256, "mixture"),   # stress workload's map and d
+])
+def test_batched_bmu_matches_oracle(rows, cols, d, n, kind):
+    say("bmu", rows, cols, d, n, kind)
+    torch = torch_cuda()
+    X, W = _bmu_case(rows, cols, d, n, seed=rows * 31 + d)
+    m = make_map(rows, cols, d, W=W)
+    idx, idx2, d1 = m.bmu(dev(X), second=True)
+    idx = idx.cpu().numpy()
+    idx2 = idx2.cpu().numpy()
+    d1 = d1.cpu().numpy()
+    ev = oracle.evaluate(W.astype(np.float64), rows, cols, X)
+    g1 = rel_gap(ev["d1"], ev["d2"])
+    sure = g1 > GAP
+    assert sure.mean() > 0.5
+    assert np.array_equal(idx[sure], ev["c1"][sure])
+    # everywhere: the chosen unit is within the gap of the true minimum
+    assert np.all(np.abs(d1 - ev["d1"]) <= 1e-5 * np.maximum(ev["d1"], 1e-3) + 1e-6)
+    if rows * cols == 1:
+        assert np.all(idx2 == -1)
+    else:
+        # second BMU: exact where both of its gaps are clear
+        D = np.stack([oracle.distances(W.astype(np.float64), X[i]) for i in range(n)])
+        Ds = np.sort(D, axis=1)
+        g2 = (Ds[:, 2] - Ds[:, 1]) / np.maximum(Ds[:, 1], 1e-300) if D.shape[1] > 2 \
+            else np.full(n, np.inf)
+        sure2 = sure & (g2 > GAP)
+        assert np.array_equal(idx2[sure2], ev["c2"][sure2])
+    # som_bmu alone gives the same indices
+    only = m.bmu(dev(X)).cpu().numpy()
+    assert np.array_equal(only, idx)
+    torch.cuda.synchronize()
+    m.close()
+
+
+def test_exact_ties_resolve_to_lowest_index_on_gpu():
+    W = np.array([[0.5, 0.5, 0, 0], [1, 0, 0, 0], [0.5, 0.5, 0, 0], [1, 0, 0, 0]],
+                 dtype=np.float32)
+    X = np.array([[0.5, 0.5, 0, 0], [1, 0, 0, 0], [0.75, 0.25, 0, 0]], dtype=np.float32)
+    m = make_map(2, 2, 4, W=W)
+    idx, idx2, _ = m.bmu(dev(X), second=True)
+    assert idx.cpu().tolist() == [0, 1, 0]
+    assert idx2.cpu().tolist() == [2, 3, 1]
+    m.close()
+
+
+# ------------------------------------------------------------ one step
+@pytest.mark.parametrize("ci", [0, 1, 2, 3, 4])
+def test_single_step_update_matches_oracle(ci):
+    """Criterion (2): one step from identical state, mid-schedule."""
+    cfg = config(ci)
+    say("single-step", cfg.name)
+    X = workloads.make_data(cfg)
+    rng = np.random.default_rng(ci)
+    N = cfg.units
+    # identical starting state: a partly trained-looking map
+    W = oracle.init_uniform(cfg.init_seed, N, cfg.d).astype(np.float32)
+    pick = rng.integers(0, cfg.n, size=N)
+    W = (0.5 * W * 0.05 + 0.5 * X[pick]).astype(np.float32)
+    i = int(rng.integers(0, cfg.n))
+    T = cfg.steps
+    for t in (0, T // 3, T - 1):
+        m = make_map(cfg.rows, cfg.cols, cfg.d, W=W)
+        # a one-step call of a T-step schedule: epochs * n must be 1 -> n = 1
+        x1 = X[i:i + 1]
+        trace = dev(np.full(1, -7, dtype=np.int32))
+        m.train(dev(x1), 1, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1,
+                order=dev(np.zeros(1, dtype=np.int32)), step0=t, total_steps=T,
+                bmu_trace=trace)
+        got = m.weights.cpu().numpy()
+        c_gpu = int(trace.cpu().numpy()[0])
+        Wo, tr = oracle.train(W.astype(np.float64), cfg.rows, cfg.cols, x1,
+                              np.zeros(1, dtype=np.int32), oracle_schedule(cfg),
+                              step0=t, total_steps=T, trace=True)
+        ev = oracle.evaluate(W.astype(np.float64), cfg.rows, cfg.cols, x1)
+        if rel_gap(ev["d1"], ev["d2"])[0] > GAP:
+            assert c_gpu == tr[0]
+        if c_gpu == tr[0]:
+            err = np.abs(got.astype(np.float64) - Wo).max()
+            say(f"  t={t} bmu={c_gpu} max|dW|={err:.2e}")
+            assert err <= STEP_ATOL
+        m.close()
+
+
+def test_radius_zero_unit_rate_copies_sample_exactly():
+    X = workloads.gaussian_mixture(6, 37, 2, 0.3, seed=2)
+    W = workloads.random_weights(12, 37, 3)
+    m = make_map(3, 4, 37, W=W)
+    trace = dev(np.full(1, -1, dtype=np.int32))
+    m.train(dev(X[4:5]), 1, 1.0, 1.0, 0.0, 0.0, order=dev(np.zeros(1, np.int32)),
+            bmu_trace=trace)
+    got = m.weights.cpu().numpy()
+    c = int(trace.cpu().numpy()[0])
+    assert c == int(np.argmin(((X[4].astype(np.float64) - W) ** 2).sum(1)))
+    assert np.array_equal(got[c], X[4])
+    others = np.arange(12) != c
+    assert np.array_equal(got[others], W[others])
+    m.close()
+
+
+def test_radius_zero_moves_only_bmu_by_lr_times_difference():
+    rng = np.random.default_rng(4)
+    W = (rng.integers(0, 64, size=(12, 8)) / 64).astype(np.float32)
+    X = (rng.integers(0, 64, size=(1, 8)) / 64).astype(np.float32)
+    m = make_map(3, 4, 8, W=W)
+    trace = dev(np.full(1, -1, dtype=np.int32))
+    m.train(dev(X), 1, 0.25, 0.25, 0.0, 0.0, order=dev(np.zeros(1, np.int32)),
+            bmu_trace=trace)
+    got = m.weights.cpu().numpy()
+    c = int(trace.cpu().numpy()[0])
+    want = W.copy()
+    want[c] = W[c] + 0.25 * (X[0] - W[c])   # exact: dyadic values
+    assert np.array_equal(got, want)
+    m.close()
+
+
+def test_infinite_radius_moves_every_unit_alike():
+    W = workloads.random_weights(6, 10, 9)
+    X = workloads.random_weights(1, 10, 10)
+    m = make_map(2, 3, 10, W=W)
+    m.train(dev(X), 1, 0.375, 0.375, math.inf, math.inf, order=dev(np.zeros(1, np.int32)))
+    got = m.weights.cpu().numpy().astype(np.float64)
+    want = W + 0.375 * (X[0] - W)
+    assert np.abs(got - want).max() <= 1e-6
+    m.close()
+
+
+# ------------------------------------------------------------ trajectories
+@pytest.mark.parametrize("ci,steps,topology", [(0, 2000, som.RECT), (1, 600, som.RECT),
+                                               (0, 400, som.HEX)])
+def test_bmu_trajectory_matches_oracle_until_first_near_tie(ci, steps, topology):
+    cfg = config(ci)
+    say("trajectory", cfg.name, steps, "hex" if topology else "rect")
+    X = workloads.make_data(cfg)
+    order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)[:steps]
+    T = cfg.steps
+    W0 = oracle.init_uniform(cfg.init_seed, cfg.units, cfg.d)
+    m = som.Map(cfg.rows, cfg.cols, cfg.d, seed=cfg.init_seed, topology=topology)
+    trace = dev(np.full(steps, -1, dtype=np.int32))
+    # som_train runs epochs * n steps: present the prefix as `steps` rows
+    Xp = dev(X[order])
+    m.train(Xp, 1, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1,
+            order=dev(np.arange(steps, dtype=np.int32)), total_steps=T, bmu_trace=trace)
+    got = trace.cpu().numpy()
+    Wo, tr = oracle.train(W0, cfg.rows, cfg.cols, X, order, oracle_schedule(cfg),
+                          total_steps=T, topology=topology, trace=True)
+    first_diff = int(np.argmax(got != tr)) if np.any(got != tr) else steps
+    say(f"  identical BMUs for {first_diff}/{steps} steps")
+    if first_diff < steps:
+        # a divergence is only allowed at a near tie of the oracle
+        Wk, _ = oracle.train(W0, cfg.rows, cfg.cols, X, order[:first_diff],
+                             oracle_schedule(cfg), total_steps=T, topology=topology)
+        D = oracle.distances(Wk, X[order[first_diff]])
+        Ds = np.sort(D)
+        assert (Ds[1] - Ds[0]) / Ds[0] <= GAP, "divergence without a near tie"
+    else:
+        err = np.abs(m.weights.cpu().numpy().astype(np.float64) - Wo).max()
+        say(f"  final max|dW| = {err:.2e}")
+        assert err <= 1e-4
+    m.close()
+
+
+def test_resume_and_determinism_are_bitwise():
+    cfg = config(0)
+    X = dev(workloads.make_data(cfg))
+    order = workloads.epoch_orders(cfg.n, 5, 0)
+    o = dev(order)
+    kw = dict(lr0=0.5, lr1=0.01, sigma0=5.0, sigma1=1.0)
+    a = som.Map(10, 10, cfg.d, seed=0)
+    a.train(X, 5, order=o, **kw)
+    b = som.Map(10, 10, cfg.d, seed=0)
+    b.train(X, 5, order=o, **kw)
+    c = som.Map(10, 10, cfg.d, seed=0)
+    T = 5 * cfg.n
+    c.train(X, 2, order=dev(order[:2 * cfg.n]), total_steps=T, **kw)
+    c.train(X, 3, order=dev(order[2 * cfg.n:]), step0=2 * cfg.n, total_steps=T, **kw)
+    wa, wb, wc = a.weights.cpu().numpy(), b.weights.cpu().numpy(), c.weights.cpu().numpy()
+    assert np.array_equal(wa, wb)
+    assert np.array_equal(wa, wc)
+    for m in (a, b, c):
+        m.close()
+
+
+def test_library_shuffle_equals_explicit_order():
+    cfg = config(0)
+    X = dev(workloads.make_data(cfg))
+    kw = dict(lr0=0.5, lr1=0.01, sigma0=5.0, sigma1=1.0)
+    order = np.concatenate([oracle.shuffle(11, e, cfg.n) for e in range(3)])
+    a = som.Map(10, 10, cfg.d, seed=1)
+    a.train(X, 3, shuffle_seed=11, **kw)
+    b = som.Map(10, 10, cfg.d, seed=1)
+    b.train(X, 3, order=dev(order), **kw)
+    assert np.array_equal(a.weights.cpu().numpy(), b.weights.cpu().numpy())
+    a.close()
+    b.close()
+
+
+# ------------------------------------------------------------ QE / TE
+@pytest.mark.parametrize("rows,cols,d,n,topology", [(10, 10, 500, 200, som.RECT),
+                                                    (8, 9, 37, 300, som.HEX),
+                                                    (1, 1, 12, 20, som.RECT)])
+def test_qe_te_of_given_weights_match_oracle(rows, cols, d, n, topology):
+    X, W = _bmu_case(rows, cols, d, n, seed=d, kind="mixture")
+    m = make_map(rows, cols, d, topology=topology, W=W)
+    qe = m.qe(dev(X))
+    te = m.te(dev(X))
+    ev = oracle.evaluate(W.astype(np.float64), rows, cols, X, topology=topology)
+    assert qe == pytest.approx(ev["qe"], rel=1e-5)
+    assert abs(te - ev["te"]) <= 1.0 / n + 1e-12
+    if rows * cols == 1:
+        assert te == 0.0
+    m.close()
+
+
+# ------------------------------------------------------------ errors
+def test_argument_and_order_errors():
+    torch = torch_cuda()
+    m = som.Map(4, 4, 8)
+    X = dev(np.zeros((10, 8), np.float32))
+    with pytest.raises(ValueError):
+        m.train(torch.zeros((10, 7), device="cuda"), 1, 0.1, 0.1, 1.0, 1.0)
+    with pytest.raises(som.SomError) as e:
+        # no device allocation covers 2^28 rows of 8 floats (8 GiB)
+        som.som_train(m.handle, X, 1 << 28, 1, som.make_schedule(0.1, 0.1, 1.0, 1.0))
+    assert e.value.name == "SOM_E_ARG"
+    with pytest.raises(som.SomError) as e:
+        m.train(X, 1, -0.1, 0.1, 1.0, 1.0)
+    assert e.value.name == "SOM_E_ARG"
+    with pytest.raises(som.SomError) as e:
+        m.train(X, 1, 0.1, 0.1, 0.0, 1.0, sigma_decay=som.EXPONENTIAL)
+    assert e.value.name == "SOM_E_ARG"
+    host = np.zeros((10, 8), np.float32)
+    with pytest.raises(som.SomError) as e:
+        som.som_train(m.handle, host.ctypes.data, 10, 1, som.make_schedule(0.1, 0.1, 1, 1))
+    assert e.value.name == "SOM_E_ARG"          # host pointer refused
+    before = m.weights.cpu().numpy()
+    bad = dev(np.array([0, 1, 2, 3, 4, 5, 6, 7, 8, 10], np.int32))
+    m.train(X, 1, 0.5, 0.5, 1.0, 1.0, order=bad)
+    with pytest.raises(som.SomError) as e:
+        m.synchronize()
+    assert e.value.name == "SOM_E_BAD_ORDER"
+    assert np.array_equal(m.weights.cpu().numpy(), before)   # nothing was updated
+    m.synchronize()                                           # error was reported once
+    m.close()
+
+
+def test_tiny_and_ragged_maps_train_like_the_oracle():
+    """Fewer units than workgroups, one-unit map, d not a multiple of 4."""
+    for rows, cols, d, n in ((1, 1, 5, 9), (2, 3, 37, 40), (1, 300, 3, 50)):
+        say("ragged", rows, cols, d, n)
+        X = workloads.gaussian_mixture(n, d, 3, 0.1, seed=d)
+        order = workloads.epoch_orders(n, 2, 1)
+        W0 = oracle.init_uniform(2, rows * cols, d)
+        m = som.Map(rows, cols, d, seed=2)
+        trace = dev(np.full(2 * n, -1, np.int32))
+        m.train(dev(X), 2, 0.5, 0.05, 2.0, 0.5, order=dev(order), bmu_trace=trace)
+        Wo, tr = oracle.train(W0, rows, cols, X, order, oracle.schedule(0.5, 0.05, 2.0, 0.5),
+                              trace=True)
+        got = trace.cpu().numpy()
+        if np.array_equal(got, tr):
+            assert np.abs(m.weights.cpu().numpy() - Wo).max() <= 1e-4
+        else:
+            k = int(np.argmax(got != tr))
+            Wk, _ = oracle.train(W0, rows, cols, X, order[:k],
+                                 oracle.schedule(0.5, 0.05, 2.0, 0.5), total_steps=2 * n)
+            Ds = np.sort(oracle.distances(Wk, X[order[k]]))
+            assert (Ds[1] - Ds[0]) / Ds[0] <= GAP
+        m.close()
