@@ -1,0 +1,190 @@
+#!/usr/bin/env python3
+"""Throughput of online SOM training on one MI355X.
+
+One bench step is one pass of the whole hot path over the workload:
+reset the map to its seeded initial prototypes, train it for the workload's
+full schedule (epochs * n per-sample steps in one persistent kernel), then
+assign every sample to its BMU and compute QE and TE (batched MFMA BMU).
+Data, order and initial prototypes are resident in HBM before timing starts.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload I]
+
+prints one JSON line.  `value` is prototype*dim updates per second of the
+whole step, T * N * d / step time.  `roofline` reports the training
+kernel: algorithmic bytes 3 * N * d * 4 per sample (read the prototypes for
+the distance, read and write them for the update) divided by the kernel's
+average duration from HIP events on its stream, against the 8 TB/s HBM peak.
+`cpu_baseline` times the fp64 oracle on the host over a bounded prefix of
+the same training run.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "train_kernel_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_1905_09598_amd", "csrc", "som_train.hip")
+
+
+def kernel_source_sha() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(workload: str):
+    """Counter-measured HBM bytes per launch, if taken on this kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = rec.get(workload)
+    if not ent or ent.get("kernel_sha256") != kernel_source_sha():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(cfg, X, order, budget_s: float):
+    """fp64 oracle on the host over a prefix of the same training run."""
+    import numpy as np
+    import oracle
+
+    threads = oracle.default_threads()
+    W = oracle.init_uniform(cfg.init_seed, cfg.units, cfg.d)
+    s = oracle.schedule(cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1,
+                        oracle.LINEAR, oracle.EXPONENTIAL)
+    done, chunk = 0, 200
+    t0 = time.perf_counter()
+    while done < cfg.steps and time.perf_counter() - t0 < budget_s:
+        k = min(chunk, cfg.steps - done)
+        W, _ = oracle.train(W, cfg.rows, cfg.cols, X, order[done:done + k], s,
+                            step0=done, total_steps=cfg.steps, nthreads=threads)
+        done += k
+    dt = time.perf_counter() - t0
+    del np
+    return {
+        "value": done * cfg.units * cfg.d / dt,
+        "unit": "proto*dim updates/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"first {done} of {cfg.steps} training steps of {cfg.name} "
+                  f"(fp64, {threads} OpenMP threads, {dt:.1f} s)",
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=1,
+                    help="index into the workload table (default: 2000 x 2000 TF-IDF)")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle time for the CPU baseline (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not "
+              "supported (the path would shard prototype rows across GPUs with one "
+              "8-byte arg-min exchange per step, which is not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_1905_09598_amd as som
+    import workloads
+
+    cfg = workloads.CONFIGS[args.workload]
+    X = workloads.make_data(cfg)
+    order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)
+    torch.cuda.set_device(0)
+    Xd = torch.from_numpy(X).cuda()
+    od = torch.from_numpy(order).cuda()
+    m = som.Map(cfg.rows, cfg.cols, cfg.d, seed=cfg.init_seed)
+    W0 = m.weights.clone()
+    plan = m.plan()
+    stream = torch.cuda.current_stream()
+
+    def one_step(ev=None):
+        m.weights = W0
+        if ev is not None:
+            ev[0].record(stream)
+        m.train(Xd, cfg.epochs, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1, order=od)
+        if ev is not None:
+            ev[1].record(stream)
+        idx = m.bmu(Xd)
+        qe, te = m.qe(Xd), m.te(Xd)
+        return idx, qe, te
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        _, qe, te = one_step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    train_ms = [a.elapsed_time(b) for a, b in events]
+    avg_train_s = sum(train_ms) / len(train_ms) / 1e3
+    updates = cfg.steps * cfg.units * cfg.d
+    ms_per_step = wall / args.steps * 1e3
+    alg_bytes = cfg.steps * 3.0 * cfg.units * cfg.d * 4
+    achieved = alg_bytes / avg_train_s / 1e9
+    traffic = measured_traffic(cfg.name)
+
+    out = {
+        "metric": "SOM train prototype*dim updates/sec + % of HBM/MALL roofline, 1 MI355X",
+        "value": updates / (ms_per_step / 1e3),
+        "unit": "proto*dim updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": cfg.name, "n": cfg.n, "d": cfg.d,
+            "map": f"{cfg.rows}x{cfg.cols}", "epochs": cfg.epochs,
+            "train_steps_per_pass": cfg.steps,
+            "schedule": f"lr {cfg.lr0}->{cfg.lr1} linear, sigma {cfg.sigma0}->{cfg.sigma1} exp",
+            "grid": plan["grid"], "block": plan["block"],
+            "variant": ["stream", "lds"][plan["variant"]],
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+            "kernel": "train_stream_kernel",
+            "kernel_ms": avg_train_s * 1e3,
+            "alg_bytes_per_launch": alg_bytes,
+        },
+        "train_ms": avg_train_s * 1e3,
+        "us_per_sample_step": avg_train_s / cfg.steps * 1e6,
+        "qe": qe,
+        "te": te,
+    }
+    if args.cpu_budget > 0:
+        out["cpu_baseline"] = cpu_baseline(cfg, X, order, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+    m.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -29,6 +29,9 @@ struct som_map {
     int64_t order_cap = 0;
     int32_t *order_host = nullptr;  // pinned
     hipEvent_t order_done = nullptr;
+    // per-step schedule table of the current training call
+    float2 *sched = nullptr;
+    int64_t sched_cap = 0;
     // evaluation scratch
     float *wnorm = nullptr;
     int32_t *cand = nullptr, *idx1 = nullptr, *idx2 = nullptr;
@@ -116,9 +119,9 @@ void fisher_yates(uint64_t seed, int64_t epoch, int64_t n, int32_t *out) {
     }
 }
 
+// Replace *p by a fresh device array of `count` elements.
 template <typename T>
-som_status grow(T **p, int64_t *cap_bytes_unused, int64_t count) {
-    (void)cap_bytes_unused;
+som_status grow(T **p, int64_t count) {
     if (*p) {
         hipError_t e = hipFree(*p);
         *p = nullptr;
@@ -132,10 +135,10 @@ som_status ensure_eval_scratch(som_map *m, int64_t n) {
     hipError_t e = hipStreamSynchronize(m->stream);
     if (e != hipSuccess) return from_hip(e);
     som_status st;
-    if ((st = grow(&m->cand, nullptr, n * som::kCand)) != SOM_OK) return st;
-    if ((st = grow(&m->idx1, nullptr, n)) != SOM_OK) return st;
-    if ((st = grow(&m->idx2, nullptr, n)) != SOM_OK) return st;
-    if ((st = grow(&m->d1, nullptr, n)) != SOM_OK) return st;
+    if ((st = grow(&m->cand, n * som::kCand)) != SOM_OK) return st;
+    if ((st = grow(&m->idx1, n)) != SOM_OK) return st;
+    if ((st = grow(&m->idx2, n)) != SOM_OK) return st;
+    if ((st = grow(&m->d1, n)) != SOM_OK) return st;
     m->eval_cap = n;
     return SOM_OK;
 }
@@ -262,6 +265,7 @@ som_status som_destroy(som_map *m) {
     (void)hipFree(m->order_dev);
     if (m->order_host) (void)hipHostFree(m->order_host);
     if (m->order_done) (void)hipEventDestroy(m->order_done);
+    (void)hipFree(m->sched);
     (void)hipFree(m->wnorm);
     (void)hipFree(m->cand);
     (void)hipFree(m->idx1);
@@ -308,9 +312,15 @@ static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
     a.slots = m->slots;
     a.state = m->state;
     a.x_vec4 = (m->d % 4 == 0) && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
+    // Launch-shape overrides for tuning sweeps: workgroup count and variant
+    // (1 = LDS-resident prototypes, 2 = streamed prototypes).
     const char *g = getenv("SOM_TRAIN_GRID");
     a.grid = (g && *g) ? atoi(g) : 0;
+    if (a.grid < 0) a.grid = 0;
     if (a.grid > m->nslots / 2) a.grid = m->nslots / 2;
+    const char *v = getenv("SOM_TRAIN_VARIANT");
+    a.variant = (v && *v) ? atoi(v) : 0;
+    if (a.variant < 0 || a.variant > 2) a.variant = 0;
     a.timeout_ticks = 100000000ull * 20;  // 20 s at the 100 MHz reference clock
     return a;
 }
@@ -399,7 +409,18 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
     a.lr_decay = s->lr_decay;
     a.sigma_decay = s->sigma_decay;
     a.bmu_trace = s->bmu_trace;
-    e = som::launch_prepare_train(order, nsteps, n, m->slots, m->nslots, m->state, m->stream);
+    if (m->sched_cap < nsteps) {
+        e = hipStreamSynchronize(m->stream);
+        if (e == hipSuccess && m->sched) e = hipFree(m->sched);
+        m->sched = nullptr;
+        m->sched_cap = 0;
+        if (e == hipSuccess)
+            e = hipMalloc(reinterpret_cast<void **>(&m->sched), (size_t)nsteps * sizeof(float2));
+        if (e != hipSuccess) return from_hip(e);
+        m->sched_cap = nsteps;
+    }
+    a.sched = m->sched;
+    e = som::launch_prepare_train(a, m->sched, m->nslots, m->stream);
     if (e == hipSuccess) e = som::launch_train(a, plan, m->stream);
     return from_hip(e);
 }

@@ -30,10 +30,12 @@ struct TrainArgs {
     int64_t nsteps, step0, total_steps;
     double lr0, lr1, sigma0, sigma1;
     int32_t lr_decay, sigma_decay;
+    const float2 *sched;    // nsteps (lr, log2(e) / (2 sigma^2)) of the call's steps
     int32_t *bmu_trace;     // nullable, nsteps entries
     unsigned long long *slots;  // 2 * grid exchange slots
     DevState *state;
-    int32_t grid;
+    int32_t grid;           // requested workgroups (0 = planner's choice)
+    int32_t variant;        // requested variant: 0 any, 1 LDS-resident, 2 streamed
     int32_t x_vec4;         // X rows may be read as float4 (d % 4 == 0, aligned)
     uint64_t timeout_ticks; // bound of one exchange wait, in 100 MHz ticks
 };
@@ -41,7 +43,7 @@ struct TrainArgs {
 struct TrainPlan {
     int32_t grid = 0;
     int32_t block = kTrainBlock;
-    int32_t variant = 0;     // 0 = streamed prototypes
+    int32_t variant = 0;     // 0 = streamed prototypes, 1 = LDS-resident
     int32_t kslots = 0;      // float4 columns per lane (template instance)
     size_t lds_bytes = 0;
 };
@@ -68,9 +70,11 @@ hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s
 
 hipError_t launch_init_uniform(float *W, int64_t ld, int32_t N, int32_t d,
                                uint64_t seed, hipStream_t s);
-hipError_t launch_prepare_train(const int32_t *order, int64_t nsteps, int64_t n,
-                                unsigned long long *slots, int32_t nslots,
-                                DevState *state, hipStream_t s);
+// Before every training launch: zero the exchange slots and the order flag,
+// then range-check the order (raising order_bad and the sticky status) and
+// fill the per-step schedule table from the fp64 decay laws.
+hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, int32_t nslots,
+                                hipStream_t s);
 hipError_t launch_row_sqnorm(const float *W, int64_t ld, int32_t N, float *out,
                              hipStream_t s);
 

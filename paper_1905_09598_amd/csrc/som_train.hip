@@ -4,26 +4,32 @@
 // runs three kernels and a host round trip per sample; here the per-sample
 // loop never leaves the device).  Each workgroup owns a fixed, contiguous
 // range of prototype rows for the whole launch, so a row is only ever read
-// and written by one workgroup (and so by one XCD and its L2).
+// and written by one workgroup (and so by one XCD and its L2).  The rows
+// live either in device memory, swept every step (variant "stream"), or in
+// the workgroup's LDS for the whole launch, loaded at the start and written
+// back at the end (variant "lds", when the slice fits).
 //
 // Step s of the call (global step t = step0 + s) with BMU c_s known:
-//   1. h_u = lr(t) exp(-|pos(u) - pos(c_s)|^2 / (2 sigma(t)^2)) for the owned
-//      rows, in fp64, rounded to fp32 (Eq. (1) with a Gaussian kernel);
+//   1. h_u = lr(t) 2^(-g(u, c_s) * log2(e) / (2 sigma(t)^2)) for the owned
+//      rows (Eq. (1) with a Gaussian kernel; lr(t) and the exponent scale
+//      come from a per-step table built in fp64 before the launch);
 //   2. one sweep over the owned rows that applies Eq. (1),
 //      w <- fma(h, x_s, fma(-h, w, w)), and in the same pass accumulates
 //      the squared distance of the updated row to the next sample x_{s+1};
 //   3. the workgroup's (distance, unit) minimum goes to a grid exchange and
 //      every workgroup reads all minima, so each learns c_{s+1} on its own.
-// A distance-only sweep before step 0 gives c_0.
+// A distance-only sweep before step 0 gives c_0.  Sample rows are loaded two
+// steps ahead so their latency hides behind the sweep and the exchange.
 //
 // The grid exchange uses one 64-bit slot per workgroup and parity,
 // dist_bits << 32 | tag << 24 | unit, written and polled with relaxed
-// device-scope atomics only.  The minimum over slots with the current tag is
-// the minimum over (distance, unit): squared distances are non-negative, so
-// their IEEE bits order like the values, and equal distances fall to the
-// lowest unit.  Slots alternate by step parity, so a fast workgroup can
-// publish step e+1 while a slow one still reads step e.  Every wait is
-// bounded in time and also ends when any workgroup has flagged an error.
+// device-scope atomics only (no fences, so no cache write-back or
+// invalidation).  The minimum over slots with the current tag is the
+// minimum over (distance, unit): squared distances are non-negative, so their
+// IEEE bits order like the values, and equal distances fall to the lowest
+// unit.  Slots alternate by step parity, so a fast workgroup can publish step
+// e+1 while a slow one still reads step e.  Every wait is bounded in time and
+// also ends when any workgroup has flagged an error.
 #include "som_internal.h"
 
 #include <math.h>
@@ -35,17 +41,27 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = kTrainBlock / 64;
 constexpr int32_t kStatusTimeout = 5;  // SOM_E_TIMEOUT
+constexpr int kHeader = 64;            // LDS bytes for the broadcast words
 
-__device__ inline double decay_at(double a, double b, int kind, double p) {
-    if (a == b) return a;
-    if (kind == 0) return (1.0 - p) * a + p * b;
-    return pow(a, 1.0 - p) * pow(b, p);
+// Sum over the 64 lanes of a wave, returned to every lane.  Within each row
+// of 16 lanes a butterfly of DPP moves (quad swaps, half-row and row
+// mirrors) leaves the row's sum in all of its lanes, bit-identical because
+// every pairwise add is commutative; the four row sums are then read out and
+// added in a fixed order.
+template <int CTRL>
+__device__ inline float dpp_pair(float v) {
+    return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
 }
-
 __device__ inline float wave_sum(float v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
+    v = dpp_pair<0xB1>(v);   // quad_perm [1,0,3,2]
+    v = dpp_pair<0x4E>(v);   // quad_perm [2,3,0,1]
+    v = dpp_pair<0x141>(v);  // row_half_mirror
+    v = dpp_pair<0x140>(v);  // row_mirror
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return (r0 + r1) + (r2 + r3);
 }
 
 __device__ inline unsigned long long u64_min(unsigned long long a, unsigned long long b) {
@@ -60,20 +76,6 @@ __device__ inline unsigned long long wave_min_u64(unsigned long long v) {
         v = u64_min(v, ((unsigned long long)hi << 32) | lo);
     }
     return v;
-}
-
-// Minimum of one value per thread over the workgroup; every thread gets it.
-__device__ inline unsigned long long block_min_u64(unsigned long long v,
-                                                   unsigned long long *red) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    v = wave_min_u64(v);
-    if (lane == 0) red[wave] = v;
-    __syncthreads();
-    unsigned long long m = red[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) m = u64_min(m, red[w]);
-    __syncthreads();
-    return m;
 }
 
 template <int K>
@@ -102,17 +104,57 @@ __device__ inline void load_sample(f4 (&x)[K], const TrainArgs &a, int64_t i,
     }
 }
 
-__device__ inline int64_t sample_at(const TrainArgs &a, int64_t s) {
-    int64_t i = a.order[s];
-    // The order was range-checked before launch; keep every read in bounds.
-    return (i >= 0 && i < a.n) ? i : 0;
+// Per-step inputs (sample index, schedule entry) are fetched 64 steps at a
+// time: lane l of a window holds the entry of step base + l, loaded with one
+// vector load, and a step's entry is read out with readlane.  Vector loads
+// keep these fetches off the scalar-memory counter that LDS operations
+// share, so waiting for LDS never waits for them.  The next window is
+// loaded while the current one is in use.
+__device__ inline int fetch_entry(const TrainArgs &a, int64_t s, int) {
+    int i = s < a.nsteps ? a.order[s] : 0;
+    return (i >= 0 && (int64_t)i < a.n) ? i : 0;  // range-checked before launch
+}
+__device__ inline float2 fetch_entry(const TrainArgs &a, int64_t s, float2) {
+    return s < a.nsteps ? a.sched[s] : make_float2(0.f, 0.f);
 }
 
-// One pass over the workgroup's rows [r0, r0 + R).  UPD applies Eq. (1) with
-// the factors in hs[]; DIST accumulates |xb - w|^2 of the (updated) rows
-// into part[r * kWaves + wave].
+template <typename T>
+struct StepWindow {
+    int64_t base;
+    T cur, next;
+
+    __device__ void init(const TrainArgs &a, int64_t b) {
+        base = b;
+        cur = fetch_entry(a, b + (threadIdx.x & 63), T());
+        next = fetch_entry(a, b + 64 + (threadIdx.x & 63), T());
+    }
+    // Entry of step s, for non-decreasing s >= base.
+    __device__ T get(const TrainArgs &a, int64_t s) {
+        if (s >= base + 64) {
+            base += 64;
+            cur = next;
+            next = fetch_entry(a, base + 64 + (threadIdx.x & 63), T());
+        }
+        return lane_value((int)(s - base));
+    }
+    __device__ T lane_value(int l) const;
+};
+
+template <>
+__device__ inline int StepWindow<int>::lane_value(int l) const {
+    return __builtin_amdgcn_readlane(cur, l);
+}
+template <>
+__device__ inline float2 StepWindow<float2>::lane_value(int l) const {
+    return make_float2(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(cur.x), l)),
+                       __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cur.y), l)));
+}
+
+// One pass over the workgroup's rows (R rows of ld4 float4 from `rows`).
+// UPD applies Eq. (1) with the factors in hs[]; DIST accumulates |xb - w|^2
+// of the (updated) rows into part[r * kWaves + wave].
 template <int K, int U, bool UPD, bool DIST>
-__device__ inline void sweep(f4 *__restrict__ W4, int64_t ld4, int r0, int R,
+__device__ inline void sweep(f4 *__restrict__ rows, int64_t ld4, int R,
                              const f4 (&xa)[K], const f4 (&xb)[K],
                              const float *hs, float *part) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -121,7 +163,7 @@ __device__ inline void sweep(f4 *__restrict__ W4, int64_t ld4, int r0, int R,
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int r = rb + u;
-            const f4 *row = W4 + (int64_t)(r0 + r) * ld4;
+            const f4 *row = rows + (int64_t)r * ld4;
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 int64_t q = tid + (int64_t)kTrainBlock * k;
@@ -132,7 +174,7 @@ __device__ inline void sweep(f4 *__restrict__ W4, int64_t ld4, int r0, int R,
         for (int u = 0; u < U; ++u) {
             const int r = rb + u;
             if (r < R) {
-                f4 *row = W4 + (int64_t)(r0 + r) * ld4;
+                f4 *row = rows + (int64_t)r * ld4;
                 const float h = UPD ? hs[r] : 0.f;
                 float acc = 0.f;
 #pragma unroll
@@ -163,43 +205,45 @@ __device__ inline void sweep(f4 *__restrict__ W4, int64_t ld4, int r0, int R,
     }
 }
 
-// Workgroup minimum of (distance, unit) over the owned rows, as a packed key.
-__device__ inline unsigned long long local_best(int r0, int R, const float *part,
-                                                unsigned long long *red) {
+struct Bcast {
+    unsigned long long key;
+    int abort;
+};
+
+// Wave 0 only: the workgroup's best (distance, unit) from the row partials,
+// published to grid exchange number e, then the minimum over every
+// workgroup's slot, left in bc->key (bc->abort set if the wait was given up).
+__device__ inline void exchange_wave0(const TrainArgs &a, int64_t e, int r0, int R,
+                                      const float *part, Bcast *bc) {
+    const int lane = threadIdx.x & 63, G = a.grid;
     unsigned long long best = ~0ull;
-    for (int r = threadIdx.x; r < R; r += kTrainBlock) {
+    for (int r = lane; r < R; r += 64) {
         float D = part[r * kWaves + 0];
 #pragma unroll
         for (int w = 1; w < kWaves; ++w) D += part[r * kWaves + w];
-        unsigned long long key =
-            ((unsigned long long)__float_as_uint(D) << 32) | (unsigned)(r0 + r);
-        best = u64_min(best, key);
+        best = u64_min(best, ((unsigned long long)__float_as_uint(D) << 32) | (unsigned)(r0 + r));
     }
-    return block_min_u64(best, red);
-}
-
-// Grid exchange number e: publish this workgroup's key, wait for every
-// workgroup's, return the winning unit (or -1 if the wait was abandoned).
-__device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long key,
-                               unsigned long long *red) {
-    const int tid = threadIdx.x, G = a.grid;
+    best = wave_min_u64(best);
     const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
     unsigned long long *slots = a.slots + (e & 1) * (int64_t)G;
-    if (tid == 0) {
-        unsigned long long v = (key & 0xffffffff00000000ull) |
-                               ((unsigned long long)tag << kUnitBits) |
-                               (key & (unsigned long long)kMaxUnits);
-        __hip_atomic_store(slots + blockIdx.x, v, __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+    if (G == 1) {
+        if (lane == 0) { bc->key = best; bc->abort = 0; }
+        return;
+    }
+    if (lane == 0) {
+        const unsigned long long v = (best & 0xffffffff00000000ull) |
+                                     ((unsigned long long)tag << kUnitBits) |
+                                     (best & (unsigned long long)kMaxUnits);
+        __hip_atomic_store(slots + blockIdx.x, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     unsigned long long m = ~0ull;
     int abort = 0;
-    for (int i = tid; i < G && !abort; i += kTrainBlock) {
+    for (int i = lane; i < G && !abort; i += 64) {
         const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
         unsigned spins = 0;
         for (;;) {
-            unsigned long long v = __hip_atomic_load(slots + i, __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
+            const unsigned long long v =
+                __hip_atomic_load(slots + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (((unsigned)(v >> kUnitBits) & 0xffu) == tag) {
                 m = u64_min(m, v);
                 break;
@@ -211,107 +255,138 @@ __device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long
                     break;
                 }
                 if (__builtin_amdgcn_s_memrealtime() - t0 > a.timeout_ticks) {
-                    __hip_atomic_store(&a.state->status, kStatusTimeout,
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(&a.state->status, kStatusTimeout, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
                     abort = 1;
                     break;
                 }
             }
-            __builtin_amdgcn_s_sleep(1);
         }
     }
-    if (__syncthreads_or(abort)) return -1;
-    m = block_min_u64(m, red);
-    return (int)(m & (unsigned long long)kMaxUnits);
+    m = wave_min_u64(m);
+    const unsigned long long any_abort = __ballot(abort);
+    if (lane == 0) { bc->key = m; bc->abort = any_abort != 0; }
 }
 
-template <int K, int U>
-__global__ __launch_bounds__(kTrainBlock, 1) void train_stream_kernel(TrainArgs a) {
+// h for the owned rows [r0, r0 + R) given BMU c (threads r < R).
+__device__ inline void neighbourhood(const TrainArgs &a, int r0, int R, int c,
+                                     float lr, float c2, float *hs) {
+    const int cr = c / a.cols, cc = c - cr * a.cols;
+    for (int r = threadIdx.x; r < R; r += kTrainBlock) {
+        const int u = r0 + r;
+        const int ur = u / a.cols, uc = u - ur * a.cols;
+        const float dr = (float)(ur - cr);
+        float g;
+        if (a.topology == 1) {
+            // odd rows shifted by 1/2, rows sqrt(3)/2 apart: dy^2 = 3/4 dr^2
+            const float dx = (float)(uc - cc) + 0.5f * (float)((ur & 1) - (cr & 1));
+            g = 0.75f * dr * dr + dx * dx;
+        } else {
+            const float dx = (float)(uc - cc);
+            g = dr * dr + dx * dx;
+        }
+        hs[r] = lr * exp2f(-g * c2);
+    }
+}
+
+template <int K, int U, bool LDSW>
+__global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const int G = a.grid, b = blockIdx.x;
+    const int G = a.grid, b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6;
     const int r0 = (int)(((int64_t)b * a.N) / G);
     const int r1 = (int)(((int64_t)(b + 1) * a.N) / G);
     const int R = r1 - r0;
-    unsigned long long *red = reinterpret_cast<unsigned long long *>(smem);
-    float *hs = reinterpret_cast<float *>(smem + 64);
-    float *part = hs + ((R + 3) & ~3);
+    const int Rp = (R + 3) & ~3;
+    Bcast *bc = reinterpret_cast<Bcast *>(smem);
+    float *hs = reinterpret_cast<float *>(smem + kHeader);
+    float *part = hs + Rp;
+    f4 *lw = reinterpret_cast<f4 *>(part + (int64_t)Rp * kWaves);
 
     if (a.state->order_bad) return;  // same value for every workgroup
     if (a.nsteps <= 0) return;
 
     const int64_t ld4 = a.ld / 4;
-    f4 *W4 = reinterpret_cast<f4 *>(a.W);
-    f4 xa[K], xb[K];
+    f4 *gw = reinterpret_cast<f4 *>(a.W) + (int64_t)r0 * ld4;
+    f4 *rows = gw;
+    if (LDSW) {
+        for (int64_t e = tid; e < (int64_t)R * ld4; e += kTrainBlock) lw[e] = gw[e];
+        rows = lw;
+    }
+
+    f4 xa[K], xb[K], xc[K];
 #pragma unroll
     for (int k = 0; k < K; ++k) xa[k] = f4{0.f, 0.f, 0.f, 0.f};
+    StepWindow<int> ow;      // sample indices, read two steps ahead
+    StepWindow<float2> sw;   // schedule entries
+    ow.init(a, 0);
+    sw.init(a, 0);
 
     // Prologue: distance-only sweep against the first sample gives c_0.
-    load_sample<K>(xb, a, sample_at(a, 0), ld4);
-    sweep<K, U, false, true>(W4, ld4, r0, R, xa, xb, hs, part);
+    load_sample<K>(xb, a, ow.get(a, 0), ld4);
+    load_sample<K>(xc, a, a.nsteps > 1 ? ow.get(a, 1) : 0, ld4);
+    if (LDSW) __syncthreads();
+    sweep<K, U, false, true>(rows, ld4, R, xa, xb, hs, part);
     __syncthreads();
-    int c = exchange(a, 0, local_best(r0, R, part, red), red);
-    if (c < 0) return;
+    if (wave == 0) exchange_wave0(a, 0, r0, R, part, bc);
+    __syncthreads();
+    if (bc->abort) return;
+    int c = (int)(bc->key & (unsigned long long)kMaxUnits);
 
-    const double T1 = (double)(a.total_steps - 1);
     for (int64_t s = 0; s < a.nsteps; ++s) {
-        if (b == 0 && threadIdx.x == 0 && a.bmu_trace) a.bmu_trace[s] = c;
+        if (b == 0 && tid == 0 && a.bmu_trace) a.bmu_trace[s] = c;
+        // rotate the sample pipeline: xa = x_s, xb = x_{s+1}, xc <- x_{s+2}
 #pragma unroll
-        for (int k = 0; k < K; ++k) xa[k] = xb[k];
+        for (int k = 0; k < K; ++k) { xa[k] = xb[k]; xb[k] = xc[k]; }
         const bool has_next = s + 1 < a.nsteps;
-        if (has_next) load_sample<K>(xb, a, sample_at(a, s + 1), ld4);
+        if (s + 2 < a.nsteps) load_sample<K>(xc, a, ow.get(a, s + 2), ld4);
+        const float2 cur = sw.get(a, s);
 
-        // Schedule and neighbourhood factors of the owned rows (fp64).
-        const int64_t t = a.step0 + s;
-        const double p = (a.total_steps > 1) ? (double)t / T1 : 0.0;
-        const double lr = decay_at(a.lr0, a.lr1, a.lr_decay, p);
-        const double sg = decay_at(a.sigma0, a.sigma1, a.sigma_decay, p);
-        for (int r = threadIdx.x; r < R; r += kTrainBlock) {
-            const int u = r0 + r;
-            double h;
-            if (sg == 0.0) {
-                h = (u == c) ? lr : 0.0;
-            } else if (isinf(sg)) {
-                h = lr;
-            } else {
-                h = lr * exp(-lattice_sq(u, c, a.cols, a.topology) / (2.0 * sg * sg));
-            }
-            hs[r] = (float)h;
-        }
+        neighbourhood(a, r0, R, c, cur.x, cur.y, hs);
         __syncthreads();
 
         if (has_next) {
-            sweep<K, U, true, true>(W4, ld4, r0, R, xa, xb, hs, part);
+            sweep<K, U, true, true>(rows, ld4, R, xa, xb, hs, part);
             __syncthreads();
-            c = exchange(a, s + 1, local_best(r0, R, part, red), red);
-            if (c < 0) return;
+            if (wave == 0) exchange_wave0(a, s + 1, r0, R, part, bc);
+            __syncthreads();
+            if (bc->abort) return;
+            c = (int)(bc->key & (unsigned long long)kMaxUnits);
         } else {
-            sweep<K, U, true, false>(W4, ld4, r0, R, xa, xb, hs, part);
+            sweep<K, U, true, false>(rows, ld4, R, xa, xb, hs, part);
         }
+    }
+    if (LDSW) {
+        __syncthreads();
+        for (int64_t e = tid; e < (int64_t)R * ld4; e += kTrainBlock) gw[e] = lw[e];
     }
 }
 
+// Row unroll of the streamed sweep: enough 16-byte loads in flight per lane.
 template <int K>
-constexpr int unroll_for() {
+constexpr int stream_unroll() {
     return K <= 2 ? 8 : (K <= 4 ? 4 : (K <= 8 ? 2 : 1));
+}
+template <int K>
+constexpr int lds_unroll() {
+    return K <= 2 ? 4 : (K <= 4 ? 2 : 1);
 }
 
 typedef void (*TrainKernel)(TrainArgs);
 
-template <int K>
-TrainKernel kernel_for() {
-    return train_stream_kernel<K, unroll_for<K>()>;
-}
-
 struct Instance {
     int k;
-    TrainKernel fn;
+    TrainKernel stream, lds;
 };
 
+template <int K>
+constexpr Instance instance() {
+    return Instance{K, train_kernel<K, stream_unroll<K>(), false>,
+                    train_kernel<K, lds_unroll<K>(), true>};
+}
+
 const Instance kInstances[] = {
-    {1, kernel_for<1>()},   {2, kernel_for<2>()},   {3, kernel_for<3>()},
-    {4, kernel_for<4>()},   {5, kernel_for<5>()},   {6, kernel_for<6>()},
-    {8, kernel_for<8>()},   {10, kernel_for<10>()}, {12, kernel_for<12>()},
-    {16, kernel_for<16>()},
+    instance<1>(), instance<2>(), instance<3>(),  instance<4>(),  instance<5>(),
+    instance<6>(), instance<8>(), instance<10>(), instance<12>(), instance<16>(),
 };
 
 const Instance *pick(int64_t ld4) {
@@ -320,27 +395,82 @@ const Instance *pick(int64_t ld4) {
     return nullptr;
 }
 
+size_t lds_bytes_for(int rmax, int64_t ld4, bool ldsw) {
+    const size_t rp = (size_t)((rmax + 3) & ~3);
+    size_t b = kHeader + rp * 4 + rp * kWaves * 4;
+    if (ldsw) b += (size_t)rmax * (size_t)ld4 * 16;
+    return b;
+}
+
+// Estimated microseconds per step (model fitted to MI355X measurements of
+// the exchange and of LDS / memory sweeps); only ranks launch shapes.
+double exchange_us(int g) { return g <= 1 ? 0.2 : 0.6 + 0.3 * log2((double)g); }
+
 }  // namespace
 
 hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
-    const Instance *in = pick(a.ld / 4);
+    const int64_t ld4 = a.ld / 4;
+    const Instance *in = pick(ld4);
     if (!in) return hipErrorInvalidValue;
-    int grid = a.grid > 0 ? a.grid : num_cus;
-    if (grid > a.N) grid = a.N;
+    int max_lds = 0;
+    hipError_t e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, 0);
+    if (e != hipSuccess) return e;
+    const int max_grid = a.N < num_cus ? a.N : num_cus;
+    const double row_bytes = 2.0 * 16.0 * (double)ld4;  // read + write per row per step
+
+    int grid = 0, variant = 0;
+    if (a.grid > 0) {
+        grid = a.grid < a.N ? a.grid : a.N;
+        const int rmax = (a.N + grid - 1) / grid;
+        variant = (a.variant != 0 && lds_bytes_for(rmax, ld4, true) <= (size_t)max_lds) ? 1 : 0;
+        if (a.variant == 1 && variant == 0) return hipErrorInvalidValue;
+    } else {
+        // streamed sweep over the whole chip: about 30 GB/s per CU of memory
+        // traffic (measured at MALL-resident sizes) plus the exchange
+        double best = 1e300;
+        {
+            const int g = max_grid;
+            const int rmax = (a.N + g - 1) / g;
+            best = exchange_us(g) + rmax * row_bytes / 30e3 + 0.5;
+            grid = g;
+            variant = 0;
+        }
+        if (a.variant != 2) {
+            // LDS-resident slices: ~300 GB/s of LDS traffic per CU
+            for (int g = 1; g <= max_grid; g *= 2) {
+                const int gg = g;
+                const int rmax = (a.N + gg - 1) / gg;
+                if (lds_bytes_for(rmax, ld4, true) > (size_t)max_lds) continue;
+                const double t = exchange_us(gg) + rmax * row_bytes / 300e3 + 0.3;
+                if (t < best) { best = t; grid = gg; variant = 1; }
+            }
+            if (variant == 1) {
+                // a non-power-of-two grid up to the CU count may fit better
+                const int g = max_grid;
+                const int rmax = (a.N + g - 1) / g;
+                if (lds_bytes_for(rmax, ld4, true) <= (size_t)max_lds) {
+                    const double t = exchange_us(g) + rmax * row_bytes / 300e3 + 0.3;
+                    if (t < best) { best = t; grid = g; }
+                }
+            }
+        }
+    }
     if (grid < 1) grid = 1;
     const int rmax = (a.N + grid - 1) / grid;
-    size_t need = 64 + (size_t)((rmax + 3) & ~3) * 4 + (size_t)rmax * kWaves * 4;
+    size_t lds = lds_bytes_for(rmax, ld4, variant == 1);
+    if (lds > (size_t)max_lds) return hipErrorInvalidValue;
     // More than half of the CU's LDS keeps one workgroup per CU, so the
     // grid spreads over every CU instead of doubling up on some.
-    size_t lds = need > 84 * 1024 ? need : 84 * 1024;
+    if (lds < 84 * 1024) lds = 84 * 1024;
+    TrainKernel fn = variant ? in->lds : in->stream;
     int per_cu = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &per_cu, reinterpret_cast<const void *>(in->fn), kTrainBlock, lds);
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(fn),
+                                                     kTrainBlock, lds);
     if (e != hipSuccess) return e;
     if (per_cu < 1 || grid > per_cu * num_cus) return hipErrorCooperativeLaunchTooLarge;
     plan->grid = grid;
     plan->block = kTrainBlock;
-    plan->variant = 0;
+    plan->variant = variant;
     plan->kslots = in->k;
     plan->lds_bytes = lds;
     return hipSuccess;
@@ -351,10 +481,10 @@ hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s
     if (!in || in->k != plan.kslots) return hipErrorInvalidValue;
     TrainArgs args = a;
     args.grid = plan.grid;
+    TrainKernel fn = plan.variant ? in->lds : in->stream;
     void *params[] = {&args};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(in->fn),
-                                      dim3(plan.grid), dim3(plan.block), params,
-                                      (unsigned)plan.lds_bytes, s);
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),
+                                      dim3(plan.block), params, (unsigned)plan.lds_bytes, s);
 }
 
 }  // namespace som

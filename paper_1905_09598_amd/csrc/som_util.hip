@@ -1,5 +1,6 @@
 // Small helper kernels: prototype initialisation, per-call preparation of
-// the training kernel's exchange slots and order check, row squared norms.
+// the training kernel (exchange slots, order check, schedule table), row
+// squared norms.
 #include "som_internal.h"
 
 namespace som {
@@ -30,24 +31,49 @@ __global__ void init_uniform_kernel(float *W, int64_t ld, int32_t N, int32_t d,
     }
 }
 
-// One workgroup: zero the exchange slots and set state->order_bad to
-// whether any order entry lies outside [0, n) (also raising the sticky
-// status).  Runs before every training launch on the same stream.
-constexpr int kPrepBlock = 1024;
-__global__ __launch_bounds__(kPrepBlock) void prepare_train_kernel(
-    const int32_t *order, int64_t nsteps, int64_t n, unsigned long long *slots,
-    int32_t nslots, DevState *state) {
-    for (int i = threadIdx.x; i < nslots; i += kPrepBlock) slots[i] = 0ull;
-    int bad = 0;
-    for (int64_t k = threadIdx.x; k < nsteps; k += kPrepBlock) {
-        const int32_t v = order[k];
-        bad |= (v < 0 || (int64_t)v >= n);
+// Zero the exchange slots and the order flag (one workgroup).
+__global__ void reset_train_kernel(unsigned long long *slots, int32_t nslots,
+                                   DevState *state) {
+    for (int i = threadIdx.x; i < nslots; i += blockDim.x) slots[i] = 0ull;
+    if (threadIdx.x == 0) state->order_bad = 0;
+}
+
+__device__ inline double decay_at(double a, double b, int kind, double p) {
+    if (a == b) return a;
+    // p = 0 gives a and p = 1 gives b exactly
+    if (kind == 0) return (1.0 - p) * a + p * b;
+    return pow(a, 1.0 - p) * pow(b, p);
+}
+
+// Per local step s: range-check order[s]; sched[s] = (lr(t), log2(e) / (2
+// sigma(t)^2)) at global step t = step0 + s, p = t / (T - 1) (p = 0 when
+// T = 1).  sigma = 0 gives the largest finite scale (a delta at the BMU),
+// sigma = +inf gives 0 (h = lr everywhere).
+__global__ void prepare_train_kernel(const int32_t *order, int64_t nsteps, int64_t n,
+                                     int64_t step0, int64_t total, double lr0, double lr1,
+                                     int lr_kind, double s0, double s1, int s_kind,
+                                     float2 *sched, DevState *state) {
+    const int64_t s = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (s >= nsteps) return;
+    const int32_t v = order[s];
+    if (v < 0 || (int64_t)v >= n) {
+        atomicOr(&state->order_bad, 1);
+        atomicCAS(&state->status, 0, 7);  // SOM_E_BAD_ORDER unless an error is pending
     }
-    bad = __syncthreads_or(bad);
-    if (threadIdx.x == 0) {
-        state->order_bad = bad;
-        if (bad) state->status = 7;  // SOM_E_BAD_ORDER
+    const int64_t t = step0 + s;
+    const double p = total > 1 ? (double)t / (double)(total - 1) : 0.0;
+    const double lr = decay_at(lr0, lr1, lr_kind, p);
+    const double sg = decay_at(s0, s1, s_kind, p);
+    double c2;
+    if (sg == 0.0) {
+        c2 = 3.4028234663852886e38;  // FLT_MAX
+    } else if (isinf(sg)) {
+        c2 = 0.0;
+    } else {
+        c2 = 1.4426950408889634 / (2.0 * sg * sg);  // log2(e) / (2 sigma^2)
+        if (c2 > 3.4028234663852886e38) c2 = 3.4028234663852886e38;
     }
+    sched[s] = make_float2((float)lr, (float)c2);
 }
 
 // out[u] = sum_j W[u][j]^2, one wave per row (fp32, fixed order).
@@ -75,11 +101,15 @@ hipError_t launch_init_uniform(float *W, int64_t ld, int32_t N, int32_t d,
     return hipGetLastError();
 }
 
-hipError_t launch_prepare_train(const int32_t *order, int64_t nsteps, int64_t n,
-                                unsigned long long *slots, int32_t nslots,
-                                DevState *state, hipStream_t s) {
-    prepare_train_kernel<<<dim3(1), dim3(kPrepBlock), 0, s>>>(order, nsteps, n, slots,
-                                                              nslots, state);
+hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, int32_t nslots,
+                                hipStream_t s) {
+    reset_train_kernel<<<dim3(1), dim3(1024), 0, s>>>(a.slots, nslots, a.state);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t blocks = (a.nsteps + 255) / 256;
+    prepare_train_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(
+        a.order, a.nsteps, a.n, a.step0, a.total_steps, a.lr0, a.lr1, a.lr_decay, a.sigma0,
+        a.sigma1, a.sigma_decay, sched, a.state);
     return hipGetLastError();
 }
 
