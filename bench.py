@@ -87,7 +87,19 @@ def main():
                     help="index into the workload table (default: 2000 x 2000 TF-IDF)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (the "
+                         "reference dispatch for scaling HBM byte counters) and exit")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes_read": n * 4, "calibrate_copy_bytes_written": n * 4}))
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not "
               "supported (the path would shard prototype rows across GPUs with one "
@@ -100,7 +112,7 @@ def main():
     import paper_1905_09598_amd as som
     import workloads
 
-    cfg = workloads.CONFIGS[args.workload]
+    cfg = workloads.WORKLOADS[args.workload]
     X = workloads.make_data(cfg)
     order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)
     torch.cuda.set_device(0)
@@ -171,7 +183,7 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
-            "kernel": "train_stream_kernel",
+            "kernel": f"train_kernel (variant {['stream', 'lds'][plan['variant']]})",
             "kernel_ms": avg_train_s * 1e3,
             "alg_bytes_per_launch": alg_bytes,
         },

@@ -43,39 +43,63 @@ constexpr int kWaves = kTrainBlock / 64;
 constexpr int32_t kStatusTimeout = 5;  // SOM_E_TIMEOUT
 constexpr int kHeader = 64;            // LDS bytes for the broadcast words
 
-// Sum over the 64 lanes of a wave, returned to every lane.  Within each row
-// of 16 lanes a butterfly of DPP moves (quad swaps, half-row and row
-// mirrors) leaves the row's sum in all of its lanes, bit-identical because
-// every pairwise add is commutative; the four row sums are then read out and
-// added in a fixed order.
+// Sums over the 64 lanes of a wave, for U values at once, returned to every
+// lane.  Within each row of 16 lanes a butterfly of DPP moves (quad swaps,
+// half-row and row mirrors) leaves the row's sum in all of its lanes,
+// bit-identical because every pairwise add is commutative; the four row sums
+// are then read out and added in a fixed order.  The U chains run in
+// lockstep so their DPP hazards overlap.
+template <int CTRL>
+__device__ inline int dpp_move(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
+}
 template <int CTRL>
 __device__ inline float dpp_pair(float v) {
-    return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+    return v + __int_as_float(dpp_move<CTRL>(__float_as_int(v)));
 }
-__device__ inline float wave_sum(float v) {
-    v = dpp_pair<0xB1>(v);   // quad_perm [1,0,3,2]
-    v = dpp_pair<0x4E>(v);   // quad_perm [2,3,0,1]
-    v = dpp_pair<0x141>(v);  // row_half_mirror
-    v = dpp_pair<0x140>(v);  // row_mirror
-    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
-    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-    return (r0 + r1) + (r2 + r3);
+__device__ inline float lane_f(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+template <int U>
+__device__ inline void wave_sums(float (&v)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0xB1>(v[u]);   // quad_perm [1,0,3,2]
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x4E>(v[u]);   // quad_perm [2,3,0,1]
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x141>(v[u]);  // row_half_mirror
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x140>(v[u]);  // row_mirror
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+        v[u] = (lane_f(v[u], 0) + lane_f(v[u], 16)) + (lane_f(v[u], 32) + lane_f(v[u], 48));
 }
 
 __device__ inline unsigned long long u64_min(unsigned long long a, unsigned long long b) {
     return a < b ? a : b;
 }
 
+template <int CTRL>
+__device__ inline unsigned long long dpp_min_u64(unsigned long long v) {
+    const unsigned lo = (unsigned)dpp_move<CTRL>((int)(unsigned)(v & 0xffffffffu));
+    const unsigned hi = (unsigned)dpp_move<CTRL>((int)(unsigned)(v >> 32));
+    return u64_min(v, ((unsigned long long)hi << 32) | lo);
+}
+
+__device__ inline unsigned long long lane_u64(unsigned long long v, int l) {
+    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(v & 0xffffffffu), l);
+    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(v >> 32), l);
+    return ((unsigned long long)hi << 32) | lo;
+}
+
+// Minimum over the 64 lanes of a wave (same DPP pattern), to every lane.
 __device__ inline unsigned long long wave_min_u64(unsigned long long v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-        unsigned lo = __shfl_xor((unsigned)(v & 0xffffffffu), o, 64);
-        unsigned hi = __shfl_xor((unsigned)(v >> 32), o, 64);
-        v = u64_min(v, ((unsigned long long)hi << 32) | lo);
-    }
-    return v;
+    v = dpp_min_u64<0xB1>(v);
+    v = dpp_min_u64<0x4E>(v);
+    v = dpp_min_u64<0x141>(v);
+    v = dpp_min_u64<0x140>(v);
+    return u64_min(u64_min(lane_u64(v, 0), lane_u64(v, 16)),
+                   u64_min(lane_u64(v, 32), lane_u64(v, 48)));
 }
 
 template <int K>
@@ -151,11 +175,12 @@ __device__ inline float2 StepWindow<float2>::lane_value(int l) const {
 }
 
 // One pass over the workgroup's rows (R rows of ld4 float4 from `rows`).
-// UPD applies Eq. (1) with the factors in hs[]; DIST accumulates |xb - w|^2
-// of the (updated) rows into part[r * kWaves + wave].
+// UPD applies Eq. (1) with row r's factor (lane r of hl when R <= 64, else
+// hs[r]); DIST accumulates |xb - w|^2 of the (updated) rows into
+// part[r * kWaves + wave].
 template <int K, int U, bool UPD, bool DIST>
 __device__ inline void sweep(f4 *__restrict__ rows, int64_t ld4, int R,
-                             const f4 (&xa)[K], const f4 (&xb)[K],
+                             const f4 (&xa)[K], const f4 (&xb)[K], float hl,
                              const float *hs, float *part) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int rb = 0; rb < R; rb += U) {
@@ -170,13 +195,15 @@ __device__ inline void sweep(f4 *__restrict__ rows, int64_t ld4, int R,
                 w[u][k] = (r < R && q < ld4) ? row[q] : f4{0.f, 0.f, 0.f, 0.f};
             }
         }
+        float acc[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int r = rb + u;
+            acc[u] = 0.f;
             if (r < R) {
                 f4 *row = rows + (int64_t)r * ld4;
-                const float h = UPD ? hs[r] : 0.f;
-                float acc = 0.f;
+                float h = 0.f;
+                if (UPD) h = (R <= 64) ? lane_f(hl, r) : hs[r];
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
                     int64_t q = tid + (int64_t)kTrainBlock * k;
@@ -190,16 +217,20 @@ __device__ inline void sweep(f4 *__restrict__ rows, int64_t ld4, int R,
                     }
                     if (DIST) {
                         f4 df = xb[k] - v;
-                        acc = fmaf(df.x, df.x, acc);
-                        acc = fmaf(df.y, df.y, acc);
-                        acc = fmaf(df.z, df.z, acc);
-                        acc = fmaf(df.w, df.w, acc);
+                        acc[u] = fmaf(df.x, df.x, acc[u]);
+                        acc[u] = fmaf(df.y, df.y, acc[u]);
+                        acc[u] = fmaf(df.z, df.z, acc[u]);
+                        acc[u] = fmaf(df.w, df.w, acc[u]);
                     }
                 }
-                if (DIST) {
-                    acc = wave_sum(acc);
-                    if (lane == 0) part[r * kWaves + wave] = acc;
-                }
+            }
+        }
+        if (DIST) {
+            wave_sums<U>(acc);
+            if (lane == 0) {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (rb + u < R) part[(rb + u) * kWaves + wave] = acc[u];
             }
         }
     }
@@ -268,25 +299,22 @@ __device__ inline void exchange_wave0(const TrainArgs &a, int64_t e, int r0, int
     if (lane == 0) { bc->key = m; bc->abort = any_abort != 0; }
 }
 
-// h for the owned rows [r0, r0 + R) given BMU c (threads r < R).
-__device__ inline void neighbourhood(const TrainArgs &a, int r0, int R, int c,
-                                     float lr, float c2, float *hs) {
-    const int cr = c / a.cols, cc = c - cr * a.cols;
-    for (int r = threadIdx.x; r < R; r += kTrainBlock) {
-        const int u = r0 + r;
-        const int ur = u / a.cols, uc = u - ur * a.cols;
-        const float dr = (float)(ur - cr);
-        float g;
-        if (a.topology == 1) {
-            // odd rows shifted by 1/2, rows sqrt(3)/2 apart: dy^2 = 3/4 dr^2
-            const float dx = (float)(uc - cc) + 0.5f * (float)((ur & 1) - (cr & 1));
-            g = 0.75f * dr * dr + dx * dx;
-        } else {
-            const float dx = (float)(uc - cc);
-            g = dr * dr + dx * dx;
-        }
-        hs[r] = lr * exp2f(-g * c2);
+// Neighbourhood factor of owned row r given BMU c: lr * 2^(-g * c2) with g
+// the squared lattice distance.  pos[r] holds (row, column, row parity) of
+// unit r0 + r.  RECT: g = dr^2 + dc^2.  HEX: odd rows shifted by 1/2 and rows
+// sqrt(3)/2 apart, so g = 3/4 dr^2 + (dc + (parity difference) / 2)^2, exact
+// in fp32 for the map sizes the library accepts.
+__device__ inline float neighbour_h(const TrainArgs &a, float4 p, float cr, float cc,
+                                    float cpar, float lr, float c2) {
+    const float dr = p.x - cr;
+    float dx = p.y - cc, g;
+    if (a.topology == 1) {
+        dx += 0.5f * (p.z - cpar);
+        g = 0.75f * dr * dr + dx * dx;
+    } else {
+        g = dr * dr + dx * dx;
     }
+    return lr * exp2f(-g * c2);
 }
 
 template <int K, int U, bool LDSW>
@@ -300,11 +328,16 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
     Bcast *bc = reinterpret_cast<Bcast *>(smem);
     float *hs = reinterpret_cast<float *>(smem + kHeader);
     float *part = hs + Rp;
-    f4 *lw = reinterpret_cast<f4 *>(part + (int64_t)Rp * kWaves);
+    float4 *pos = reinterpret_cast<float4 *>(part + (int64_t)Rp * kWaves);
+    f4 *lw = reinterpret_cast<f4 *>(pos + Rp);
 
     if (a.state->order_bad) return;  // same value for every workgroup
     if (a.nsteps <= 0) return;
 
+    for (int r = tid; r < R; r += kTrainBlock) {
+        const int u = r0 + r, ur = u / a.cols, uc = u - ur * a.cols;
+        pos[r] = make_float4((float)ur, (float)uc, (float)(ur & 1), 0.f);
+    }
     const int64_t ld4 = a.ld / 4;
     f4 *gw = reinterpret_cast<f4 *>(a.W) + (int64_t)r0 * ld4;
     f4 *rows = gw;
@@ -324,8 +357,10 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
     // Prologue: distance-only sweep against the first sample gives c_0.
     load_sample<K>(xb, a, ow.get(a, 0), ld4);
     load_sample<K>(xc, a, a.nsteps > 1 ? ow.get(a, 1) : 0, ld4);
-    if (LDSW) __syncthreads();
-    sweep<K, U, false, true>(rows, ld4, R, xa, xb, hs, part);
+    __syncthreads();
+    float4 mypos = make_float4(0.f, 0.f, 0.f, 0.f);  // lane l: row l's position
+    if ((tid & 63) < R) mypos = pos[tid & 63];
+    sweep<K, U, false, true>(rows, ld4, R, xa, xb, 0.f, hs, part);
     __syncthreads();
     if (wave == 0) exchange_wave0(a, 0, r0, R, part, bc);
     __syncthreads();
@@ -341,18 +376,26 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
         if (s + 2 < a.nsteps) load_sample<K>(xc, a, ow.get(a, s + 2), ld4);
         const float2 cur = sw.get(a, s);
 
-        neighbourhood(a, r0, R, c, cur.x, cur.y, hs);
-        __syncthreads();
+        const int cr = c / a.cols, ccol = c - cr * a.cols;
+        const float fcr = (float)cr, fcc = (float)ccol, fcp = (float)(cr & 1);
+        float hl = 0.f;
+        if (R <= 64) {
+            if ((tid & 63) < R) hl = neighbour_h(a, mypos, fcr, fcc, fcp, cur.x, cur.y);
+        } else {
+            for (int r = tid; r < R; r += kTrainBlock)
+                hs[r] = neighbour_h(a, pos[r], fcr, fcc, fcp, cur.x, cur.y);
+            __syncthreads();
+        }
 
         if (has_next) {
-            sweep<K, U, true, true>(rows, ld4, R, xa, xb, hs, part);
+            sweep<K, U, true, true>(rows, ld4, R, xa, xb, hl, hs, part);
             __syncthreads();
             if (wave == 0) exchange_wave0(a, s + 1, r0, R, part, bc);
             __syncthreads();
             if (bc->abort) return;
             c = (int)(bc->key & (unsigned long long)kMaxUnits);
         } else {
-            sweep<K, U, true, false>(rows, ld4, R, xa, xb, hs, part);
+            sweep<K, U, true, false>(rows, ld4, R, xa, xb, hl, hs, part);
         }
     }
     if (LDSW) {
@@ -397,7 +440,7 @@ const Instance *pick(int64_t ld4) {
 
 size_t lds_bytes_for(int rmax, int64_t ld4, bool ldsw) {
     const size_t rp = (size_t)((rmax + 3) & ~3);
-    size_t b = kHeader + rp * 4 + rp * kWaves * 4;
+    size_t b = kHeader + rp * 4 + rp * kWaves * 4 + rp * 16;
     if (ldsw) b += (size_t)rmax * (size_t)ld4 * 16;
     return b;
 }

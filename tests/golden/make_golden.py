@@ -33,7 +33,7 @@ def main():
     ap.add_argument("--epoch-qe", action="store_true",
                     help="also record the quantization error after every epoch")
     args = ap.parse_args()
-    cfg = workloads.CONFIGS[args.config]
+    cfg = workloads.WORKLOADS[args.config]
     t0 = time.time()
     X = workloads.make_data(cfg)
     order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)

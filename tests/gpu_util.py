@@ -51,4 +51,4 @@ def say(*a):
 
 
 def config(i):
-    return workloads.CONFIGS[i]
+    return workloads.WORKLOADS[i]

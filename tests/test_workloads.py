@@ -5,9 +5,9 @@ import pytest
 import workloads as w
 
 
-def test_configs_table():
-    assert len(w.CONFIGS) == 5
-    c = w.CONFIGS
+def test_workload_table():
+    assert len(w.WORKLOADS) == 5
+    c = w.WORKLOADS
     assert (c[0].n, c[0].d, c[0].units, c[0].steps) == (200, 500, 100, 2000)
     assert (c[1].n, c[1].d, c[1].units, c[1].steps) == (2000, 2000, 400, 40000)
     assert (c[2].n, c[2].d, c[2].units, c[2].steps) == (5000, 5000, 900, 250000)
@@ -18,7 +18,7 @@ def test_configs_table():
 
 @pytest.mark.parametrize("i", [0, 1])
 def test_tfidf_rows_are_sparse_unit_norm_and_deterministic(i):
-    cfg = w.CONFIGS[i]
+    cfg = w.WORKLOADS[i]
     X = w.make_data(cfg)
     assert X.shape == (cfg.n, cfg.d) and X.dtype == np.float32
     nnz = (X != 0).sum(axis=1)

@@ -32,7 +32,7 @@ from typing import Optional
 import numpy as np
 
 __all__ = [
-    "SomConfig", "CONFIGS", "tfidf_like", "gaussian_mixture", "make_data",
+    "SomConfig", "WORKLOADS", "tfidf_like", "gaussian_mixture", "make_data",
     "epoch_orders", "sha256_of",
 ]
 
@@ -81,7 +81,7 @@ class SomConfig:
 
 # Five workloads: a tiny one the oracle finishes in well under a second, three
 # TF-IDF-shaped ones of growing size and a dense Gaussian-mixture stress case.
-CONFIGS = (
+WORKLOADS = (
     SomConfig("tfidf_n200_d500_map10x10", n=200, d=500, rows=10, cols=10,
               epochs=10, lr0=0.5, lr1=0.01, sigma0=5.0, sigma1=1.0,
               kind="tfidf", density=0.02, topics=1, data_seed=0),
@@ -217,10 +217,6 @@ def epoch_orders(n: int, epochs: int, seed: int = 0,
 
 def sha256_of(a: np.ndarray) -> str:
     return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
-
-
-def config_by_index(i: int) -> SomConfig:
-    return CONFIGS[i]
 
 
 def small_tfidf(n: int, d: int, seed: int, density: float = 0.02,
