@@ -1,7 +1,8 @@
 // Host runtime of libsom: the C ABI declared in include/som.h.
 //
-// Owns the map (prototypes in device memory, row pitch padded to a multiple
-// of 4 floats so rows can be read as 16-byte vectors), validates every
+// Owns the map (prototypes in device memory, each row padded with zeros to
+// the training kernel's lane slots, so rows are read as 16-byte vectors with
+// no column bounds), validates every
 // argument before any device work, builds the per-epoch sample order when
 // the caller gives none, and launches the kernels on the map's stream.
 #include "som.h"
@@ -217,7 +218,10 @@ som_status som_create(int32_t rows, int32_t cols, int32_t d, uint64_t seed,
     *out = nullptr;
     const int64_t N = (int64_t)rows * cols;
     if (N > som::kMaxUnits) return SOM_E_ARG;
-    const int64_t ld = ((int64_t)d + 3) / 4 * 4;
+    // Rows padded to the training kernel's lane slots (zero padding) when a
+    // kernel shape covers d; otherwise to 16 bytes (evaluation only).
+    int64_t ld = som::train_row_pitch(d);
+    if (ld == 0) ld = ((int64_t)d + 3) / 4 * 4;
     const uint64_t bytes = (uint64_t)N * (uint64_t)ld * sizeof(float);
     if (bytes / sizeof(float) / (uint64_t)ld != (uint64_t)N) return SOM_E_ARG;
     if (bytes > max_bytes()) return SOM_E_OOM;

@@ -64,6 +64,11 @@ __device__ inline double lattice_sq(int u, int c, int cols, int topology) {
     return dr * dr + dc * dc;
 }
 
+// Row pitch (floats) of a d-dimensional map: d rounded up to the training
+// kernel's lane slots (16-byte columns times lanes per row), so the sweep
+// needs no column bounds; 0 when no training kernel covers d.
+int64_t train_row_pitch(int32_t d);
+
 // Host-side launchers (each translation unit owns its kernels).
 hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan);
 hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s);

@@ -102,22 +102,30 @@ __device__ inline unsigned long long wave_min_u64(unsigned long long v) {
                    u64_min(lane_u64(v, 32), lane_u64(v, 48)));
 }
 
-template <int K>
-__device__ inline void load_sample(f4 (&x)[K], const TrainArgs &a, int64_t i,
-                                   int64_t ld4) {
-    const int tid = threadIdx.x;
+// Lane layout.  A workgroup's 256 threads form P = 256 / L groups of L
+// lanes; group g sweeps rows g, g + P, g + 2P, ... of the workgroup's slice
+// and lane j of a group holds the 16-byte columns j, j + L, ..., j + (K-1) L
+// of its rows (and of the sample rows).  With L = 64 a wave owns whole rows,
+// so a row's distance needs one wave-level reduction and nothing else; with
+// L = 256 every wave holds a quarter of every row (long rows) and the four
+// partial sums meet in LDS.
+// Sample row i into the lane's slots; columns past d (row padding) are 0.
+template <int K, int L>
+__device__ inline void load_sample(f4 (&x)[K], const TrainArgs &a, int64_t i) {
+    const int li = threadIdx.x % L;
     if (a.x_vec4) {
         const f4 *xr = reinterpret_cast<const f4 *>(a.X + i * a.d);
+        const int xd4 = a.d >> 2;  // d % 4 == 0 on this path
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-            int64_t q = tid + (int64_t)kTrainBlock * k;
-            x[k] = (q < ld4) ? xr[q] : f4{0.f, 0.f, 0.f, 0.f};
+            const int q = li + L * k;
+            x[k] = (q < xd4) ? xr[q] : f4{0.f, 0.f, 0.f, 0.f};
         }
     } else {
         const float *xr = a.X + i * a.d;
 #pragma unroll
         for (int k = 0; k < K; ++k) {
-            int64_t j = 4 * (tid + (int64_t)kTrainBlock * k);
+            const int j = 4 * (li + L * k);
             f4 v;
             v.x = (j + 0 < a.d) ? xr[j + 0] : 0.f;
             v.y = (j + 1 < a.d) ? xr[j + 1] : 0.f;
@@ -174,49 +182,57 @@ __device__ inline float2 StepWindow<float2>::lane_value(int l) const {
                        __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cur.y), l)));
 }
 
-// One pass over the workgroup's rows (R rows of ld4 float4 from `rows`).
+__device__ inline unsigned long long row_key(float D, int u) {
+    return ((unsigned long long)__float_as_uint(D) << 32) | (unsigned)u;
+}
+
+// One pass over the workgroup's R rows, each L * K float4 long (the row
+// pitch is padded to exactly the lanes' slots, padding zero), from `rows`.
 // UPD applies Eq. (1) with row r's factor (lane r of hl when R <= 64, else
-// hs[r]); DIST accumulates |xb - w|^2 of the (updated) rows into
-// part[r * kWaves + wave].
-template <int K, int U, bool UPD, bool DIST>
-__device__ inline void sweep(f4 *__restrict__ rows, int64_t ld4, int R,
-                             const f4 (&xa)[K], const f4 (&xb)[K], float hl,
-                             const float *hs, float *part) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    for (int rb = 0; rb < R; rb += U) {
+// hs[r]).  DIST accumulates |xb - w|^2 of the updated rows: with L = 64 the
+// wave's best (distance, unit) key over its rows is returned; with L = 256
+// the wave's partial sum of row r goes to part[r * 4 + wave].
+template <int K, int U, int L, bool UPD, bool DIST>
+__device__ inline unsigned long long sweep(f4 *__restrict__ rows, int r0, int R,
+                                           const f4 (&xa)[K], const f4 (&xb)[K], float hl,
+                                           const float *hs, float *part) {
+    constexpr int P = kTrainBlock / L;
+    constexpr int P4 = L * K;  // float4 per row
+    const int tid = threadIdx.x, g = tid / L, li = tid % L, lane = tid & 63;
+    const int wave = tid >> 6;
+    unsigned long long best = ~0ull;
+    for (int rb = g; rb < R; rb += P * U) {
         f4 w[U][K];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int r = rb + u;
-            const f4 *row = rows + (int64_t)r * ld4;
+            const int r = rb + u * P;
+            if (r < R) {
+                const f4 *row = rows + (size_t)r * P4 + li;
 #pragma unroll
-            for (int k = 0; k < K; ++k) {
-                int64_t q = tid + (int64_t)kTrainBlock * k;
-                w[u][k] = (r < R && q < ld4) ? row[q] : f4{0.f, 0.f, 0.f, 0.f};
+                for (int k = 0; k < K; ++k) w[u][k] = row[L * k];
             }
         }
         float acc[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int r = rb + u;
+            const int r = rb + u * P;
             acc[u] = 0.f;
             if (r < R) {
-                f4 *row = rows + (int64_t)r * ld4;
+                f4 *row = rows + (size_t)r * P4 + li;
                 float h = 0.f;
                 if (UPD) h = (R <= 64) ? lane_f(hl, r) : hs[r];
 #pragma unroll
                 for (int k = 0; k < K; ++k) {
-                    int64_t q = tid + (int64_t)kTrainBlock * k;
                     f4 v = w[u][k];
                     if (UPD) {
                         v.x = fmaf(h, xa[k].x, fmaf(-h, v.x, v.x));
                         v.y = fmaf(h, xa[k].y, fmaf(-h, v.y, v.y));
                         v.z = fmaf(h, xa[k].z, fmaf(-h, v.z, v.z));
                         v.w = fmaf(h, xa[k].w, fmaf(-h, v.w, v.w));
-                        if (q < ld4) row[q] = v;
+                        row[L * k] = v;
                     }
                     if (DIST) {
-                        f4 df = xb[k] - v;
+                        const f4 df = xb[k] - v;
                         acc[u] = fmaf(df.x, df.x, acc[u]);
                         acc[u] = fmaf(df.y, df.y, acc[u]);
                         acc[u] = fmaf(df.z, df.z, acc[u]);
@@ -227,40 +243,58 @@ __device__ inline void sweep(f4 *__restrict__ rows, int64_t ld4, int R,
         }
         if (DIST) {
             wave_sums<U>(acc);
-            if (lane == 0) {
+            if (L == 64) {
 #pragma unroll
                 for (int u = 0; u < U; ++u)
-                    if (rb + u < R) part[(rb + u) * kWaves + wave] = acc[u];
+                    if (rb + u * P < R) best = u64_min(best, row_key(acc[u], r0 + rb + u * P));
+            } else if (lane == 0) {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (rb + u * P < R) part[(rb + u * P) * kWaves + wave] = acc[u];
             }
         }
     }
+    return best;
 }
 
 struct Bcast {
     unsigned long long key;
     int abort;
+    int pad;
+    unsigned long long wave_best[kWaves];
 };
 
-// Wave 0 only: the workgroup's best (distance, unit) from the row partials,
-// published to grid exchange number e, then the minimum over every
-// workgroup's slot, left in bc->key (bc->abort set if the wait was given up).
-__device__ inline void exchange_wave0(const TrainArgs &a, int64_t e, int r0, int R,
-                                      const float *part, Bcast *bc) {
-    const int lane = threadIdx.x & 63, G = a.grid;
+// Wave 0, after the sweep's barrier: the workgroup's best (distance, unit).
+template <int L>
+__device__ inline unsigned long long workgroup_best(int r0, int R, const float *part,
+                                                    const Bcast *bc) {
+    const int lane = threadIdx.x & 63;
     unsigned long long best = ~0ull;
-    for (int r = lane; r < R; r += 64) {
-        float D = part[r * kWaves + 0];
+    if (L == 64) {
+        if (lane < kWaves) best = bc->wave_best[lane];
+    } else {
+        for (int r = lane; r < R; r += 64) {
+            float D = part[r * kWaves + 0];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) D += part[r * kWaves + w];
-        best = u64_min(best, ((unsigned long long)__float_as_uint(D) << 32) | (unsigned)(r0 + r));
+            for (int w = 1; w < kWaves; ++w) D += part[r * kWaves + w];
+            best = u64_min(best, row_key(D, r0 + r));
+        }
     }
-    best = wave_min_u64(best);
-    const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
-    unsigned long long *slots = a.slots + (e & 1) * (int64_t)G;
+    return wave_min_u64(best);
+}
+
+// Wave 0 only: publish the workgroup's best key to grid exchange number e,
+// then take the minimum over every workgroup's slot into bc->key (bc->abort
+// set if the wait was given up).
+__device__ inline void exchange_wave0(const TrainArgs &a, int64_t e,
+                                      unsigned long long best, Bcast *bc) {
+    const int lane = threadIdx.x & 63, G = a.grid;
     if (G == 1) {
         if (lane == 0) { bc->key = best; bc->abort = 0; }
         return;
     }
+    const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
+    unsigned long long *slots = a.slots + (e & 1) * (int64_t)G;
     if (lane == 0) {
         const unsigned long long v = (best & 0xffffffff00000000ull) |
                                      ((unsigned long long)tag << kUnitBits) |
@@ -317,10 +351,10 @@ __device__ inline float neighbour_h(const TrainArgs &a, float4 p, float cr, floa
     return lr * exp2f(-g * c2);
 }
 
-template <int K, int U, bool LDSW>
+template <int K, int U, int L, bool LDSW>
 __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const int G = a.grid, b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6;
+    const int G = a.grid, b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int r0 = (int)(((int64_t)b * a.N) / G);
     const int r1 = (int)(((int64_t)(b + 1) * a.N) / G);
     const int R = r1 - r0;
@@ -355,14 +389,15 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
     sw.init(a, 0);
 
     // Prologue: distance-only sweep against the first sample gives c_0.
-    load_sample<K>(xb, a, ow.get(a, 0), ld4);
-    load_sample<K>(xc, a, a.nsteps > 1 ? ow.get(a, 1) : 0, ld4);
+    load_sample<K, L>(xb, a, ow.get(a, 0));
+    load_sample<K, L>(xc, a, a.nsteps > 1 ? ow.get(a, 1) : 0);
     __syncthreads();
     float4 mypos = make_float4(0.f, 0.f, 0.f, 0.f);  // lane l: row l's position
-    if ((tid & 63) < R) mypos = pos[tid & 63];
-    sweep<K, U, false, true>(rows, ld4, R, xa, xb, 0.f, hs, part);
+    if (lane < R) mypos = pos[lane];
+    unsigned long long wb = sweep<K, U, L, false, true>(rows, r0, R, xa, xb, 0.f, hs, part);
+    if (L == 64 && lane == 0) bc->wave_best[wave] = wb;
     __syncthreads();
-    if (wave == 0) exchange_wave0(a, 0, r0, R, part, bc);
+    if (wave == 0) exchange_wave0(a, 0, workgroup_best<L>(r0, R, part, bc), bc);
     __syncthreads();
     if (bc->abort) return;
     int c = (int)(bc->key & (unsigned long long)kMaxUnits);
@@ -373,14 +408,14 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
 #pragma unroll
         for (int k = 0; k < K; ++k) { xa[k] = xb[k]; xb[k] = xc[k]; }
         const bool has_next = s + 1 < a.nsteps;
-        if (s + 2 < a.nsteps) load_sample<K>(xc, a, ow.get(a, s + 2), ld4);
+        if (s + 2 < a.nsteps) load_sample<K, L>(xc, a, ow.get(a, s + 2));
         const float2 cur = sw.get(a, s);
 
         const int cr = c / a.cols, ccol = c - cr * a.cols;
         const float fcr = (float)cr, fcc = (float)ccol, fcp = (float)(cr & 1);
         float hl = 0.f;
         if (R <= 64) {
-            if ((tid & 63) < R) hl = neighbour_h(a, mypos, fcr, fcc, fcp, cur.x, cur.y);
+            if (lane < R) hl = neighbour_h(a, mypos, fcr, fcc, fcp, cur.x, cur.y);
         } else {
             for (int r = tid; r < R; r += kTrainBlock)
                 hs[r] = neighbour_h(a, pos[r], fcr, fcc, fcp, cur.x, cur.y);
@@ -388,14 +423,15 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
         }
 
         if (has_next) {
-            sweep<K, U, true, true>(rows, ld4, R, xa, xb, hl, hs, part);
+            wb = sweep<K, U, L, true, true>(rows, r0, R, xa, xb, hl, hs, part);
+            if (L == 64 && lane == 0) bc->wave_best[wave] = wb;
             __syncthreads();
-            if (wave == 0) exchange_wave0(a, s + 1, r0, R, part, bc);
+            if (wave == 0) exchange_wave0(a, s + 1, workgroup_best<L>(r0, R, part, bc), bc);
             __syncthreads();
             if (bc->abort) return;
             c = (int)(bc->key & (unsigned long long)kMaxUnits);
         } else {
-            sweep<K, U, true, false>(rows, ld4, R, xa, xb, hl, hs, part);
+            sweep<K, U, L, true, false>(rows, r0, R, xa, xb, hl, hs, part);
         }
     }
     if (LDSW) {
@@ -404,37 +440,42 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
     }
 }
 
-// Row unroll of the streamed sweep: enough 16-byte loads in flight per lane.
+// Rows in flight per group: enough 16-byte loads outstanding per lane for
+// the streamed variant, enough independent reductions for the LDS one.
 template <int K>
 constexpr int stream_unroll() {
     return K <= 2 ? 8 : (K <= 4 ? 4 : (K <= 8 ? 2 : 1));
 }
 template <int K>
 constexpr int lds_unroll() {
-    return K <= 2 ? 4 : (K <= 4 ? 2 : 1);
+    return K <= 2 ? 4 : (K <= 8 ? 2 : 1);
 }
 
 typedef void (*TrainKernel)(TrainArgs);
 
 struct Instance {
-    int k;
+    int lanes, k;
     TrainKernel stream, lds;
 };
 
-template <int K>
+template <int L, int K>
 constexpr Instance instance() {
-    return Instance{K, train_kernel<K, stream_unroll<K>(), false>,
-                    train_kernel<K, lds_unroll<K>(), true>};
+    return Instance{L, K, train_kernel<K, stream_unroll<K>(), L, false>,
+                    train_kernel<K, lds_unroll<K>(), L, true>};
 }
 
+// Rows up to 512 float4 (d <= 2048) use wave-owned rows; longer rows span
+// the workgroup.
 const Instance kInstances[] = {
-    instance<1>(), instance<2>(), instance<3>(),  instance<4>(),  instance<5>(),
-    instance<6>(), instance<8>(), instance<10>(), instance<12>(), instance<16>(),
+    instance<64, 1>(),   instance<64, 2>(),   instance<64, 3>(),   instance<64, 4>(),
+    instance<64, 5>(),   instance<64, 6>(),   instance<64, 8>(),   instance<256, 3>(),
+    instance<256, 4>(),  instance<256, 5>(),  instance<256, 6>(),  instance<256, 8>(),
+    instance<256, 10>(), instance<256, 12>(), instance<256, 16>(),
 };
 
 const Instance *pick(int64_t ld4) {
     for (const Instance &in : kInstances)
-        if ((int64_t)in.k * kTrainBlock >= ld4) return &in;
+        if ((int64_t)in.k * in.lanes >= ld4) return &in;
     return nullptr;
 }
 
@@ -451,10 +492,15 @@ double exchange_us(int g) { return g <= 1 ? 0.2 : 0.6 + 0.3 * log2((double)g); }
 
 }  // namespace
 
+int64_t train_row_pitch(int32_t d) {
+    const Instance *in = pick(((int64_t)d + 3) / 4);
+    return in ? 4 * (int64_t)in->lanes * in->k : 0;
+}
+
 hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     const int64_t ld4 = a.ld / 4;
     const Instance *in = pick(ld4);
-    if (!in) return hipErrorInvalidValue;
+    if (!in || (int64_t)in->lanes * in->k != ld4) return hipErrorInvalidValue;
     int max_lds = 0;
     hipError_t e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, 0);
     if (e != hipSuccess) return e;
@@ -521,7 +567,8 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
 
 hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s) {
     const Instance *in = pick(a.ld / 4);
-    if (!in || in->k != plan.kslots) return hipErrorInvalidValue;
+    if (!in || in->k != plan.kslots || (int64_t)in->lanes * in->k != a.ld / 4)
+        return hipErrorInvalidValue;
     TrainArgs args = a;
     args.grid = plan.grid;
     TrainKernel fn = plan.variant ? in->lds : in->stream;
