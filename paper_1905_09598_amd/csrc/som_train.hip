@@ -5,31 +5,38 @@
 // loop never leaves the device).  Each workgroup owns a fixed, contiguous
 // range of prototype rows for the whole launch, so a row is only ever read
 // and written by one workgroup (and so by one XCD and its L2).  The rows
-// live either in device memory, swept every step (variant "stream"), or in
-// the workgroup's LDS for the whole launch, loaded at the start and written
-// back at the end (variant "lds", when the slice fits).
+// live either in device memory (variant "stream") or in the workgroup's LDS
+// for the whole launch, loaded at the start and written back at the end
+// (variant "lds", when the slice fits).
 //
-// Step s of the call (global step t = step0 + s) with BMU c_s known:
-//   1. h_u = lr(t) 2^(-g(u, c_s) * log2(e) / (2 sigma(t)^2)) for the owned
-//      rows (Eq. (1) with a Gaussian kernel; lr(t) and the exponent scale
-//      come from a per-step table built in fp64 before the launch);
-//   2. one sweep over the owned rows that applies Eq. (1),
-//      w <- fma(h, x_s, fma(-h, w, w)), and in the same pass accumulates
-//      the squared distance of the updated row to the next sample x_{s+1};
-//   3. the workgroup's (distance, unit) minimum goes to a grid exchange and
-//      every workgroup reads all minima, so each learns c_{s+1} on its own.
-// A distance-only sweep before step 0 gives c_0.  Sample rows are loaded two
-// steps ahead so their latency hides behind the sweep and the exchange.
+// Blocked sweeps.  Eq. (1) applied for steps k = 0..M-1 of a block keeps
+// every prototype an affine combination of its value W at the block start
+// and the block's samples x_0..x_{M-1}:
+//     W^(k) = beta_k W + sum_{j<k} gamma_kj x_j,   beta_k + sum_j gamma_kj = 1,
+// with beta_{k+1} = (1 - h_k) beta_k, gamma_{k+1,j} = (1 - h_k) gamma_kj and
+// gamma_{k+1,k} = h_k, h_k the unit's neighbourhood factor at step k.  So
+//     x_k - W^(k) = e_k - sum_{j<k} gamma_kj e_j,   e_j = x_j - W,
+// and the squared distance that picks step k's BMU is
+//     D_k = E_kk - 2 sum_j gamma_kj E_jk + sum_ij gamma_ki gamma_kj E_ij
+// with E the Gram matrix of the e_j, per unit.  One sweep over the owned rows
+// therefore (a) applies a whole block's updates at once,
+// w <- beta w + sum_j gamma_j x_j, and (b) accumulates the Gram matrix of the
+// next block's samples against the updated rows.  Between sweeps the M BMUs
+// of a block come from these per-unit scalars alone.  This is Eq. (1)
+// step by step in exact arithmetic, with one pass over the prototypes per M
+// samples; the first distance of each block is the plain direct-difference
+// squared distance E_00.
 //
-// The grid exchange uses one 64-bit slot per workgroup and parity,
-// dist_bits << 32 | tag << 24 | unit, written and polled with relaxed
-// device-scope atomics only (no fences, so no cache write-back or
-// invalidation).  The minimum over slots with the current tag is the
-// minimum over (distance, unit): squared distances are non-negative, so their
-// IEEE bits order like the values, and equal distances fall to the lowest
-// unit.  Slots alternate by step parity, so a fast workgroup can publish step
-// e+1 while a slow one still reads step e.  Every wait is bounded in time and
-// also ends when any workgroup has flagged an error.
+// Per step the workgroup's (distance, unit) minimum goes to a grid exchange:
+// one 64-bit slot per workgroup and parity, dist_bits << 32 | tag << 24 |
+// unit, written and polled with relaxed device-scope atomics only (no fences,
+// so no cache write-back or invalidation).  The minimum over slots with the
+// current tag is the minimum over (distance, unit): squared distances are
+// non-negative, so their IEEE bits order like the values, and equal distances
+// fall to the lowest unit.  Slots alternate by step parity, so a fast
+// workgroup can publish step e+1 while a slow one still reads step e.  Every
+// wait is bounded in time and also ends when any workgroup has flagged an
+// error.
 #include "som_internal.h"
 
 #include <math.h>
@@ -39,7 +46,6 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = kTrainBlock / 64;
 constexpr int32_t kStatusTimeout = 5;  // SOM_E_TIMEOUT
 constexpr int kHeader = 64;            // LDS bytes for the broadcast words
 
@@ -102,13 +108,6 @@ __device__ inline unsigned long long wave_min_u64(unsigned long long v) {
                    u64_min(lane_u64(v, 32), lane_u64(v, 48)));
 }
 
-// Lane layout.  A workgroup's 256 threads form P = 256 / L groups of L
-// lanes; group g sweeps rows g, g + P, g + 2P, ... of the workgroup's slice
-// and lane j of a group holds the 16-byte columns j, j + L, ..., j + (K-1) L
-// of its rows (and of the sample rows).  With L = 64 a wave owns whole rows,
-// so a row's distance needs one wave-level reduction and nothing else; with
-// L = 256 every wave holds a quarter of every row (long rows) and the four
-// partial sums meet in LDS.
 // Sample row i into the lane's slots; columns past d (row padding) are 0.
 template <int K, int L>
 __device__ inline void load_sample(f4 (&x)[K], const TrainArgs &a, int64_t i) {
@@ -182,25 +181,46 @@ __device__ inline float2 StepWindow<float2>::lane_value(int l) const {
                        __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cur.y), l)));
 }
 
+
+// Packed index of the Gram entry (i, j), i <= j.
+__device__ constexpr int tri(int i, int j) { return j * (j + 1) / 2 + i; }
+__device__ constexpr int tri_any(int i, int j) { return i <= j ? tri(i, j) : tri(j, i); }
+
 __device__ inline unsigned long long row_key(float D, int u) {
     return ((unsigned long long)__float_as_uint(D) << 32) | (unsigned)u;
 }
 
-// One pass over the workgroup's R rows, each L * K float4 long (the row
-// pitch is padded to exactly the lanes' slots, padding zero), from `rows`.
-// UPD applies Eq. (1) with row r's factor (lane r of hl when R <= 64, else
-// hs[r]).  DIST accumulates |xb - w|^2 of the updated rows: with L = 64 the
-// wave's best (distance, unit) key over its rows is returned; with L = 256
-// the wave's partial sum of row r goes to part[r * 4 + wave].
-template <int K, int U, int L, bool UPD, bool DIST>
-__device__ inline unsigned long long sweep(f4 *__restrict__ rows, int r0, int R,
-                                           const f4 (&xa)[K], const f4 (&xb)[K], float hl,
-                                           const float *hs, float *part) {
+// Lane layout.  A workgroup's 256 threads form P = 256 / L groups of L
+// lanes; group g sweeps rows g, g + P, g + 2P, ... of the workgroup's slice,
+// and lane j of a group holds the 16-byte columns j, j + L, ..., j + (K-1) L
+// of its rows and of the samples.  The row pitch is padded with zeros to
+// exactly L * K columns, so the sweep has no column bounds.
+
+// Load the M samples of the block starting at call step s_begin (steps past
+// the end load sample 0; their coefficients stay zero).
+template <int K, int L, int M>
+__device__ inline void load_block(f4 (&x)[M][K], const TrainArgs &a, int64_t s_begin,
+                                  StepWindow<int> &ow) {
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+        const int64_t s = s_begin + j;
+        const int i = (s < a.nsteps) ? ow.get(a, s) : 0;
+        load_sample<K, L>(x[j], a, i);
+    }
+}
+
+// One pass over the workgroup's R rows.  UPD applies the block's updates
+// from coef[r] = (beta, gamma_0..gamma_{M-1}); GRAM accumulates the Gram
+// matrix of e_j = xg_j - w over the (updated) row into E[r] (or, with more
+// than one wave per row, the wave's partials into part[(r * T + t) * WPR + w]).
+template <int K, int L, int M, int U, bool UPD, bool GRAM>
+__device__ inline void sweep(f4 *__restrict__ rows, int R, const f4 (&xu)[M][K],
+                             const f4 (&xg)[M][K], const float *coef, float *E, float *part) {
     constexpr int P = kTrainBlock / L;
-    constexpr int P4 = L * K;  // float4 per row
-    const int tid = threadIdx.x, g = tid / L, li = tid % L, lane = tid & 63;
-    const int wave = tid >> 6;
-    unsigned long long best = ~0ull;
+    constexpr int P4 = L * K;
+    constexpr int T = M * (M + 1) / 2;
+    constexpr int WPR = L / 64;
+    const int tid = threadIdx.x, g = tid / L, li = tid % L, lane = tid & 63, wig = li >> 6;
     for (int rb = g; rb < R; rb += P * U) {
         f4 w[U][K];
 #pragma unroll
@@ -212,87 +232,78 @@ __device__ inline unsigned long long sweep(f4 *__restrict__ rows, int r0, int R,
                 for (int k = 0; k < K; ++k) w[u][k] = row[L * k];
             }
         }
-        float acc[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int r = rb + u * P;
-            acc[u] = 0.f;
-            if (r < R) {
-                f4 *row = rows + (size_t)r * P4 + li;
-                float h = 0.f;
-                if (UPD) h = (R <= 64) ? lane_f(hl, r) : hs[r];
+            if (r >= R) continue;
+            f4 *row = rows + (size_t)r * P4 + li;
+            float beta = 1.f, gam[M];
 #pragma unroll
-                for (int k = 0; k < K; ++k) {
-                    f4 v = w[u][k];
-                    if (UPD) {
-                        v.x = fmaf(h, xa[k].x, fmaf(-h, v.x, v.x));
-                        v.y = fmaf(h, xa[k].y, fmaf(-h, v.y, v.y));
-                        v.z = fmaf(h, xa[k].z, fmaf(-h, v.z, v.z));
-                        v.w = fmaf(h, xa[k].w, fmaf(-h, v.w, v.w));
-                        row[L * k] = v;
+            for (int j = 0; j < M; ++j) gam[j] = 0.f;
+            if (UPD) {
+                beta = coef[r * (M + 1)];
+#pragma unroll
+                for (int j = 0; j < M; ++j) gam[j] = coef[r * (M + 1) + 1 + j];
+            }
+            float acc[T];
+#pragma unroll
+            for (int t = 0; t < T; ++t) acc[t] = 0.f;
+#pragma unroll
+            for (int k = 0; k < K; ++k) {
+                f4 v = w[u][k];
+                if (UPD) {
+                    v = v * beta;
+#pragma unroll
+                    for (int j = 0; j < M; ++j) {
+                        v.x = fmaf(gam[j], xu[j][k].x, v.x);
+                        v.y = fmaf(gam[j], xu[j][k].y, v.y);
+                        v.z = fmaf(gam[j], xu[j][k].z, v.z);
+                        v.w = fmaf(gam[j], xu[j][k].w, v.w);
                     }
-                    if (DIST) {
-                        const f4 df = xb[k] - v;
-                        acc[u] = fmaf(df.x, df.x, acc[u]);
-                        acc[u] = fmaf(df.y, df.y, acc[u]);
-                        acc[u] = fmaf(df.z, df.z, acc[u]);
-                        acc[u] = fmaf(df.w, df.w, acc[u]);
+                    row[L * k] = v;
+                }
+                if (GRAM) {
+                    f4 e[M];
+#pragma unroll
+                    for (int j = 0; j < M; ++j) e[j] = xg[j][k] - v;
+#pragma unroll
+                    for (int j = 0; j < M; ++j)
+#pragma unroll
+                        for (int i = 0; i <= j; ++i) {
+                            float t = acc[tri(i, j)];
+                            t = fmaf(e[i].x, e[j].x, t);
+                            t = fmaf(e[i].y, e[j].y, t);
+                            t = fmaf(e[i].z, e[j].z, t);
+                            t = fmaf(e[i].w, e[j].w, t);
+                            acc[tri(i, j)] = t;
+                        }
+                }
+            }
+            if (GRAM) {
+                wave_sums<T>(acc);
+                if (lane == 0) {
+#pragma unroll
+                    for (int t = 0; t < T; ++t) {
+                        if (WPR == 1) E[r * T + t] = acc[t];
+                        else part[(r * T + t) * WPR + wig] = acc[t];
                     }
                 }
             }
         }
-        if (DIST) {
-            wave_sums<U>(acc);
-            if (L == 64) {
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    if (rb + u * P < R) best = u64_min(best, row_key(acc[u], r0 + rb + u * P));
-            } else if (lane == 0) {
-#pragma unroll
-                for (int u = 0; u < U; ++u)
-                    if (rb + u * P < R) part[(rb + u * P) * kWaves + wave] = acc[u];
-            }
-        }
     }
-    return best;
 }
 
 struct Bcast {
-    unsigned long long key;
     int abort;
-    int pad;
-    unsigned long long wave_best[kWaves];
+    int pad[3];
 };
 
-// Wave 0, after the sweep's barrier: the workgroup's best (distance, unit).
-template <int L>
-__device__ inline unsigned long long workgroup_best(int r0, int R, const float *part,
-                                                    const Bcast *bc) {
-    const int lane = threadIdx.x & 63;
-    unsigned long long best = ~0ull;
-    if (L == 64) {
-        if (lane < kWaves) best = bc->wave_best[lane];
-    } else {
-        for (int r = lane; r < R; r += 64) {
-            float D = part[r * kWaves + 0];
-#pragma unroll
-            for (int w = 1; w < kWaves; ++w) D += part[r * kWaves + w];
-            best = u64_min(best, row_key(D, r0 + r));
-        }
-    }
-    return wave_min_u64(best);
-}
-
-// Wave 0 only: publish the workgroup's best key to grid exchange number e,
-// then take the minimum over every workgroup's slot into bc->key (bc->abort
-// set if the wait was given up).
-__device__ inline void exchange_wave0(const TrainArgs &a, int64_t e,
-                                      unsigned long long best, Bcast *bc) {
+// Wave 0 only: publish this workgroup's best key to grid exchange number e
+// and return the winning unit over every workgroup's slot (the same in all
+// lanes), or -1 if the wait was given up.
+__device__ inline int exchange_wave0(const TrainArgs &a, int64_t e, unsigned long long best) {
     const int lane = threadIdx.x & 63, G = a.grid;
-    if (G == 1) {
-        if (lane == 0) { bc->key = best; bc->abort = 0; }
-        return;
-    }
+    if (G == 1) return (int)(best & (unsigned long long)kMaxUnits);
     const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
     unsigned long long *slots = a.slots + (e & 1) * (int64_t)G;
     if (lane == 0) {
@@ -329,8 +340,8 @@ __device__ inline void exchange_wave0(const TrainArgs &a, int64_t e,
         }
     }
     m = wave_min_u64(m);
-    const unsigned long long any_abort = __ballot(abort);
-    if (lane == 0) { bc->key = m; bc->abort = any_abort != 0; }
+    if (__ballot(abort) != 0) return -1;
+    return (int)(m & (unsigned long long)kMaxUnits);
 }
 
 // Neighbourhood factor of owned row r given BMU c: lr * 2^(-g * c2) with g
@@ -351,126 +362,190 @@ __device__ inline float neighbour_h(const TrainArgs &a, float4 p, float cr, floa
     return lr * exp2f(-g * c2);
 }
 
-template <int K, int U, int L, bool LDSW>
+// Wave 0 only: the BMUs of the block's mb steps, s0 .. s0 + mb - 1, from the
+// Gram matrices E of the owned rows (LDS), leaving each row's update
+// coefficients (beta, gamma_0..) in coef.  Returns false if an exchange
+// was given up.
+template <int L, int M>
+__device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0, int R,
+                                  float *E, const float *part, float *coef, const float4 *pos,
+                                  StepWindow<float2> &sw) {
+    constexpr int T = M * (M + 1) / 2;
+    constexpr int WPR = L / 64;
+    const int lane = threadIdx.x & 63;
+    if (WPR > 1) {
+        for (int idx = lane; idx < R * T; idx += 64) {
+            float v = part[idx * WPR];
+#pragma unroll
+            for (int w = 1; w < WPR; ++w) v += part[idx * WPR + w];
+            E[idx] = v;
+        }
+    }
+    for (int r = lane; r < R; r += 64) {
+        coef[r * (M + 1)] = 1.f;
+#pragma unroll
+        for (int j = 0; j < M; ++j) coef[r * (M + 1) + 1 + j] = 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < M; ++k) {
+        if (k >= mb) break;
+        const int64_t s = s0 + k;
+        unsigned long long best = ~0ull;
+        for (int r = lane; r < R; r += 64) {
+            const float *Er = E + r * T;
+            const float *gr = coef + r * (M + 1) + 1;
+            float lin = 0.f, quad = 0.f;
+#pragma unroll
+            for (int j = 0; j < k; ++j) {
+                float inner = 0.f;
+#pragma unroll
+                for (int i = 0; i < k; ++i) inner = fmaf(gr[i], Er[tri_any(i, j)], inner);
+                lin = fmaf(gr[j], Er[tri(j, k)], lin);
+                quad = fmaf(gr[j], inner, quad);
+            }
+            const float D = fmaf(-2.f, lin, Er[tri(k, k)]) + quad;
+            best = u64_min(best, row_key(D, r0 + r));
+        }
+        best = wave_min_u64(best);
+        const int c = exchange_wave0(a, s, best);
+        if (c < 0) return false;
+        if (blockIdx.x == 0 && lane == 0 && a.bmu_trace) a.bmu_trace[s] = c;
+        const float2 sc = sw.get(a, s);
+        const int cr = c / a.cols, ccol = c - cr * a.cols;
+        const float fcr = (float)cr, fcc = (float)ccol, fcp = (float)(cr & 1);
+        for (int r = lane; r < R; r += 64) {
+            const float h = neighbour_h(a, pos[r], fcr, fcc, fcp, sc.x, sc.y);
+            const float om = 1.f - h;
+            float *cf = coef + r * (M + 1);
+            cf[0] *= om;
+#pragma unroll
+            for (int j = 0; j < k; ++j) cf[1 + j] *= om;
+            cf[1 + k] = h;
+        }
+    }
+    return true;
+}
+
+struct Layout {
+    int Rp;
+    float *E, *part, *coef;
+    float4 *pos;
+    f4 *lw;
+};
+
+template <int K, int L, int M>
+__device__ inline Layout layout(unsigned char *smem, int R) {
+    constexpr int T = M * (M + 1) / 2;
+    constexpr int WPR = L / 64;
+    Layout l;
+    l.Rp = (R + 3) & ~3;
+    unsigned char *p = smem + kHeader;
+    l.E = reinterpret_cast<float *>(p);
+    p += (size_t)l.Rp * T * 4;
+    l.part = reinterpret_cast<float *>(p);
+    if (WPR > 1) p += (size_t)l.Rp * T * WPR * 4;
+    l.coef = reinterpret_cast<float *>(p);
+    p += (size_t)l.Rp * (M + 1) * 4;
+    p = reinterpret_cast<unsigned char *>((reinterpret_cast<uintptr_t>(p) + 15) & ~(uintptr_t)15);
+    l.pos = reinterpret_cast<float4 *>(p);
+    p += (size_t)l.Rp * 16;
+    l.lw = reinterpret_cast<f4 *>(p);
+    return l;
+}
+
+// One block: its BMUs (wave 0), then one sweep that applies the block's
+// updates with samples xu and accumulates the next block's Gram matrices
+// with samples xg, then the samples of the block after next go into xu.
+template <int K, int L, int M, int U>
+__device__ inline bool run_block(const TrainArgs &a, int64_t blk, int64_t nblocks, int r0,
+                                 int R, f4 *rows, const Layout &l, f4 (&xu)[M][K],
+                                 const f4 (&xg)[M][K], StepWindow<int> &ow,
+                                 StepWindow<float2> &sw, Bcast *bc) {
+    const int wave = threadIdx.x >> 6;
+    const int64_t s0 = blk * M;
+    const int mb = (int)((a.nsteps - s0) < M ? (a.nsteps - s0) : M);
+    if (wave == 0) {
+        const bool ok = block_bmus<L, M>(a, s0, mb, r0, R, l.E, l.part, l.coef, l.pos, sw);
+        if ((threadIdx.x & 63) == 0) bc->abort = ok ? 0 : 1;
+    }
+    __syncthreads();
+    if (bc->abort) return false;
+    if (blk + 1 < nblocks)
+        sweep<K, L, M, U, true, true>(rows, R, xu, xg, l.coef, l.E, l.part);
+    else
+        sweep<K, L, M, U, true, false>(rows, R, xu, xg, l.coef, l.E, l.part);
+    if (blk + 2 < nblocks) load_block<K, L, M>(xu, a, (blk + 2) * M, ow);
+    __syncthreads();
+    return true;
+}
+
+template <int K, int L, int M, int U, bool LDSW>
 __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
-    const int G = a.grid, b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int G = a.grid, b = blockIdx.x, tid = threadIdx.x;
     const int r0 = (int)(((int64_t)b * a.N) / G);
     const int r1 = (int)(((int64_t)(b + 1) * a.N) / G);
     const int R = r1 - r0;
-    const int Rp = (R + 3) & ~3;
+    constexpr int P4 = L * K;
     Bcast *bc = reinterpret_cast<Bcast *>(smem);
-    float *hs = reinterpret_cast<float *>(smem + kHeader);
-    float *part = hs + Rp;
-    float4 *pos = reinterpret_cast<float4 *>(part + (int64_t)Rp * kWaves);
-    f4 *lw = reinterpret_cast<f4 *>(pos + Rp);
+    const Layout l = layout<K, L, M>(smem, R);
 
     if (a.state->order_bad) return;  // same value for every workgroup
     if (a.nsteps <= 0) return;
 
     for (int r = tid; r < R; r += kTrainBlock) {
         const int u = r0 + r, ur = u / a.cols, uc = u - ur * a.cols;
-        pos[r] = make_float4((float)ur, (float)uc, (float)(ur & 1), 0.f);
+        l.pos[r] = make_float4((float)ur, (float)uc, (float)(ur & 1), 0.f);
     }
-    const int64_t ld4 = a.ld / 4;
-    f4 *gw = reinterpret_cast<f4 *>(a.W) + (int64_t)r0 * ld4;
+    f4 *gw = reinterpret_cast<f4 *>(a.W) + (int64_t)r0 * P4;
     f4 *rows = gw;
     if (LDSW) {
-        for (int64_t e = tid; e < (int64_t)R * ld4; e += kTrainBlock) lw[e] = gw[e];
-        rows = lw;
+        for (int e = tid; e < R * P4; e += kTrainBlock) l.lw[e] = gw[e];
+        rows = l.lw;
     }
 
-    f4 xa[K], xb[K], xc[K];
-#pragma unroll
-    for (int k = 0; k < K; ++k) xa[k] = f4{0.f, 0.f, 0.f, 0.f};
-    StepWindow<int> ow;      // sample indices, read two steps ahead
-    StepWindow<float2> sw;   // schedule entries
+    StepWindow<int> ow;      // sample indices
+    StepWindow<float2> sw;   // schedule entries (wave 0)
     ow.init(a, 0);
     sw.init(a, 0);
-
-    // Prologue: distance-only sweep against the first sample gives c_0.
-    load_sample<K, L>(xb, a, ow.get(a, 0));
-    load_sample<K, L>(xc, a, a.nsteps > 1 ? ow.get(a, 1) : 0);
+    const int64_t nblocks = (a.nsteps + M - 1) / M;
+    f4 xA[M][K], xB[M][K];
+    load_block<K, L, M>(xA, a, 0, ow);
+    if (nblocks > 1) load_block<K, L, M>(xB, a, M, ow);
     __syncthreads();
-    float4 mypos = make_float4(0.f, 0.f, 0.f, 0.f);  // lane l: row l's position
-    if (lane < R) mypos = pos[lane];
-    unsigned long long wb = sweep<K, U, L, false, true>(rows, r0, R, xa, xb, 0.f, hs, part);
-    if (L == 64 && lane == 0) bc->wave_best[wave] = wb;
+    // Gram matrices of block 0 against the initial prototypes.
+    sweep<K, L, M, U, false, true>(rows, R, xA, xA, l.coef, l.E, l.part);
     __syncthreads();
-    if (wave == 0) exchange_wave0(a, 0, workgroup_best<L>(r0, R, part, bc), bc);
-    __syncthreads();
-    if (bc->abort) return;
-    int c = (int)(bc->key & (unsigned long long)kMaxUnits);
 
-    for (int64_t s = 0; s < a.nsteps; ++s) {
-        if (b == 0 && tid == 0 && a.bmu_trace) a.bmu_trace[s] = c;
-        // rotate the sample pipeline: xa = x_s, xb = x_{s+1}, xc <- x_{s+2}
-#pragma unroll
-        for (int k = 0; k < K; ++k) { xa[k] = xb[k]; xb[k] = xc[k]; }
-        const bool has_next = s + 1 < a.nsteps;
-        if (s + 2 < a.nsteps) load_sample<K, L>(xc, a, ow.get(a, s + 2));
-        const float2 cur = sw.get(a, s);
-
-        const int cr = c / a.cols, ccol = c - cr * a.cols;
-        const float fcr = (float)cr, fcc = (float)ccol, fcp = (float)(cr & 1);
-        float hl = 0.f;
-        if (R <= 64) {
-            if (lane < R) hl = neighbour_h(a, mypos, fcr, fcc, fcp, cur.x, cur.y);
-        } else {
-            for (int r = tid; r < R; r += kTrainBlock)
-                hs[r] = neighbour_h(a, pos[r], fcr, fcc, fcp, cur.x, cur.y);
-            __syncthreads();
-        }
-
-        if (has_next) {
-            wb = sweep<K, U, L, true, true>(rows, r0, R, xa, xb, hl, hs, part);
-            if (L == 64 && lane == 0) bc->wave_best[wave] = wb;
-            __syncthreads();
-            if (wave == 0) exchange_wave0(a, s + 1, workgroup_best<L>(r0, R, part, bc), bc);
-            __syncthreads();
-            if (bc->abort) return;
-            c = (int)(bc->key & (unsigned long long)kMaxUnits);
-        } else {
-            sweep<K, U, L, true, false>(rows, r0, R, xa, xb, hl, hs, part);
-        }
+    for (int64_t blk = 0; blk < nblocks; blk += 2) {
+        if (!run_block<K, L, M, U>(a, blk, nblocks, r0, R, rows, l, xA, xB, ow, sw, bc)) return;
+        if (blk + 1 < nblocks &&
+            !run_block<K, L, M, U>(a, blk + 1, nblocks, r0, R, rows, l, xB, xA, ow, sw, bc))
+            return;
     }
-    if (LDSW) {
-        __syncthreads();
-        for (int64_t e = tid; e < (int64_t)R * ld4; e += kTrainBlock) gw[e] = lw[e];
-    }
-}
-
-// Rows in flight per group: enough 16-byte loads outstanding per lane for
-// the streamed variant, enough independent reductions for the LDS one.
-template <int K>
-constexpr int stream_unroll() {
-    return K <= 2 ? 8 : (K <= 4 ? 4 : (K <= 8 ? 2 : 1));
-}
-template <int K>
-constexpr int lds_unroll() {
-    return K <= 2 ? 4 : (K <= 8 ? 2 : 1);
+    if (LDSW)
+        for (int e = tid; e < R * P4; e += kTrainBlock) gw[e] = l.lw[e];
 }
 
 typedef void (*TrainKernel)(TrainArgs);
 
 struct Instance {
-    int lanes, k;
+    int lanes, k, m;
     TrainKernel stream, lds;
 };
 
-template <int L, int K>
+template <int L, int K, int M, int U>
 constexpr Instance instance() {
-    return Instance{L, K, train_kernel<K, stream_unroll<K>(), L, false>,
-                    train_kernel<K, lds_unroll<K>(), L, true>};
+    return Instance{L, K, M, train_kernel<K, L, M, U, false>, train_kernel<K, L, M, U, true>};
 }
 
-// Rows up to 512 float4 (d <= 2048) use wave-owned rows; longer rows span
-// the workgroup.
+// Row pitch L * K float4 (d up to 4 L K floats) and block length M, sized so
+// the two blocks of samples (2 M K float4 per lane) stay in registers.
 const Instance kInstances[] = {
-    instance<64, 1>(),   instance<64, 2>(),   instance<64, 3>(),   instance<64, 4>(),
-    instance<64, 5>(),   instance<64, 6>(),   instance<64, 8>(),   instance<256, 3>(),
-    instance<256, 4>(),  instance<256, 5>(),  instance<256, 6>(),  instance<256, 8>(),
-    instance<256, 10>(), instance<256, 12>(), instance<256, 16>(),
+    instance<64, 1, 8, 1>(),   instance<64, 2, 8, 1>(),   instance<64, 4, 4, 1>(),
+    instance<128, 4, 4, 2>(),  instance<256, 3, 4, 1>(),  instance<256, 4, 4, 1>(),
+    instance<256, 5, 3, 1>(),  instance<256, 6, 2, 1>(),  instance<256, 8, 2, 1>(),
+    instance<256, 10, 2, 1>(), instance<256, 12, 1, 1>(), instance<256, 16, 1, 1>(),
 };
 
 const Instance *pick(int64_t ld4) {
@@ -479,10 +554,13 @@ const Instance *pick(int64_t ld4) {
     return nullptr;
 }
 
-size_t lds_bytes_for(int rmax, int64_t ld4, bool ldsw) {
+size_t lds_bytes_for(const Instance &in, int rmax, bool ldsw) {
     const size_t rp = (size_t)((rmax + 3) & ~3);
-    size_t b = kHeader + rp * 4 + rp * kWaves * 4 + rp * 16;
-    if (ldsw) b += (size_t)rmax * (size_t)ld4 * 16;
+    const size_t T = (size_t)in.m * (in.m + 1) / 2, wpr = in.lanes / 64;
+    size_t b = kHeader + rp * T * 4 + (wpr > 1 ? rp * T * wpr * 4 : 0) + rp * (in.m + 1) * 4;
+    b = (b + 15) & ~(size_t)15;
+    b += rp * 16;
+    if (ldsw) b += (size_t)rmax * in.lanes * in.k * 16;
     return b;
 }
 
@@ -505,18 +583,19 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     hipError_t e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, 0);
     if (e != hipSuccess) return e;
     const int max_grid = a.N < num_cus ? a.N : num_cus;
-    const double row_bytes = 2.0 * 16.0 * (double)ld4;  // read + write per row per step
+    // bytes moved per row per block sweep (read + write), spread over M steps
+    const double row_bytes = 2.0 * 16.0 * (double)ld4 / in->m;
 
     int grid = 0, variant = 0;
     if (a.grid > 0) {
         grid = a.grid < a.N ? a.grid : a.N;
         const int rmax = (a.N + grid - 1) / grid;
-        variant = (a.variant != 0 && lds_bytes_for(rmax, ld4, true) <= (size_t)max_lds) ? 1 : 0;
+        variant = (a.variant != 2 && lds_bytes_for(*in, rmax, true) <= (size_t)max_lds) ? 1 : 0;
         if (a.variant == 1 && variant == 0) return hipErrorInvalidValue;
     } else {
         // streamed sweep over the whole chip: about 30 GB/s per CU of memory
         // traffic (measured at MALL-resident sizes) plus the exchange
-        double best = 1e300;
+        double best;
         {
             const int g = max_grid;
             const int rmax = (a.N + g - 1) / g;
@@ -527,17 +606,16 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
         if (a.variant != 2) {
             // LDS-resident slices: ~300 GB/s of LDS traffic per CU
             for (int g = 1; g <= max_grid; g *= 2) {
-                const int gg = g;
-                const int rmax = (a.N + gg - 1) / gg;
-                if (lds_bytes_for(rmax, ld4, true) > (size_t)max_lds) continue;
-                const double t = exchange_us(gg) + rmax * row_bytes / 300e3 + 0.3;
-                if (t < best) { best = t; grid = gg; variant = 1; }
+                const int rmax = (a.N + g - 1) / g;
+                if (lds_bytes_for(*in, rmax, true) > (size_t)max_lds) continue;
+                const double t = exchange_us(g) + rmax * row_bytes / 300e3 + 0.3;
+                if (t < best) { best = t; grid = g; variant = 1; }
             }
             if (variant == 1) {
                 // a non-power-of-two grid up to the CU count may fit better
                 const int g = max_grid;
                 const int rmax = (a.N + g - 1) / g;
-                if (lds_bytes_for(rmax, ld4, true) <= (size_t)max_lds) {
+                if (lds_bytes_for(*in, rmax, true) <= (size_t)max_lds) {
                     const double t = exchange_us(g) + rmax * row_bytes / 300e3 + 0.3;
                     if (t < best) { best = t; grid = g; }
                 }
@@ -546,7 +624,7 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     }
     if (grid < 1) grid = 1;
     const int rmax = (a.N + grid - 1) / grid;
-    size_t lds = lds_bytes_for(rmax, ld4, variant == 1);
+    size_t lds = lds_bytes_for(*in, rmax, variant == 1);
     if (lds > (size_t)max_lds) return hipErrorInvalidValue;
     // More than half of the CU's LDS keeps one workgroup per CU, so the
     // grid spreads over every CU instead of doubling up on some.
