@@ -23,8 +23,7 @@ struct som_map {
     hipStream_t stream = nullptr;
     float *W = nullptr;
     som::DevState *state = nullptr;
-    unsigned long long *slots = nullptr;
-    int32_t nslots = 0;
+    unsigned long long *slots = nullptr;  // grid-exchange words
     // order staging for library-shuffled training
     int32_t *order_dev = nullptr;
     int64_t order_cap = 0;
@@ -240,12 +239,9 @@ som_status som_create(int32_t rows, int32_t cols, int32_t d, uint64_t seed,
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->W), bytes);
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->state), sizeof(som::DevState));
     if (e == hipSuccess) e = hipMemset(m->state, 0, sizeof(som::DevState));
-    if (e == hipSuccess) {
-        m->nslots = 2 * (m->num_cus > 0 ? m->num_cus : 1);
-        if (m->nslots < 2 * 1024) m->nslots = 2 * 1024;
+    if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&m->slots),
-                      (size_t)m->nslots * sizeof(unsigned long long));
-    }
+                      (size_t)som::kSlotWords * sizeof(unsigned long long));
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->wnorm), (size_t)N * sizeof(float));
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->sums), 2 * sizeof(double));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&m->order_done, hipEventDisableTiming);
@@ -321,7 +317,7 @@ static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
     const char *g = getenv("SOM_TRAIN_GRID");
     a.grid = (g && *g) ? atoi(g) : 0;
     if (a.grid < 0) a.grid = 0;
-    if (a.grid > m->nslots / 2) a.grid = m->nslots / 2;
+    if (a.grid > som::kMaxTrainGrid) a.grid = som::kMaxTrainGrid;
     const char *v = getenv("SOM_TRAIN_VARIANT");
     a.variant = (v && *v) ? atoi(v) : 0;
     if (a.variant < 0 || a.variant > 2) a.variant = 0;
@@ -424,7 +420,9 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
         m->sched_cap = nsteps;
     }
     a.sched = m->sched;
-    e = som::launch_prepare_train(a, m->sched, m->nslots, m->stream);
+    a.grid = plan.grid;
+    a.slot_spread = plan.slot_spread;
+    e = som::launch_prepare_train(a, m->sched, m->stream);
     if (e == hipSuccess) e = som::launch_train(a, plan, m->stream);
     return from_hip(e);
 }

@@ -12,6 +12,14 @@ constexpr int kTrainBlock = 256;
 // Grid-exchange slot layout: 64-bit key = dist_bits << 32 | tag << 24 | unit.
 constexpr int kUnitBits = 24;
 constexpr int32_t kMaxUnits = (1 << kUnitBits) - 1;
+// Each workgroup writes its key into kSlotReplicas copies of the slot array
+// and polls the copy of its XCD (workgroup b runs on XCD b % 8), so each
+// copy is read by one eighth of the grid; slots sit `slot_spread` u64 apart.
+constexpr int kSlotReplicas = 8;
+constexpr int kMaxTrainGrid = 1024;
+constexpr int kMaxSlotSpread = 16;
+constexpr int64_t kSlotReplicaStride = 2LL * kMaxTrainGrid * kMaxSlotSpread;  // u64
+constexpr int64_t kSlotWords = kSlotReplicas * kSlotReplicaStride;
 
 // Device-side status words of a map (one allocation, zeroed at creation).
 struct DevState {
@@ -32,7 +40,8 @@ struct TrainArgs {
     int32_t lr_decay, sigma_decay;
     const float2 *sched;    // nsteps (lr, log2(e) / (2 sigma^2)) of the call's steps
     int32_t *bmu_trace;     // nullable, nsteps entries
-    unsigned long long *slots;  // 2 * grid exchange slots
+    unsigned long long *slots;  // kSlotWords exchange words
+    int32_t slot_spread;        // u64 between consecutive workgroups' slots
     DevState *state;
     int32_t grid;           // requested workgroups (0 = planner's choice)
     int32_t variant;        // requested variant: 0 any, 1 LDS-resident, 2 streamed
@@ -45,6 +54,7 @@ struct TrainPlan {
     int32_t block = kTrainBlock;
     int32_t variant = 0;     // 0 = streamed prototypes, 1 = LDS-resident
     int32_t kslots = 0;      // float4 columns per lane (template instance)
+    int32_t slot_spread = 1;
     size_t lds_bytes = 0;
 };
 
@@ -75,11 +85,11 @@ hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s
 
 hipError_t launch_init_uniform(float *W, int64_t ld, int32_t N, int32_t d,
                                uint64_t seed, hipStream_t s);
-// Before every training launch: zero the exchange slots and the order flag,
-// then range-check the order (raising order_bad and the sticky status) and
-// fill the per-step schedule table from the fp64 decay laws.
-hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, int32_t nslots,
-                                hipStream_t s);
+// Before every training launch (a.grid and a.slot_spread set): zero the
+// exchange slots in use and the order flag, then range-check the order
+// (raising order_bad and the sticky status) and fill the per-step schedule
+// table from the fp64 decay laws.
+hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, hipStream_t s);
 hipError_t launch_row_sqnorm(const float *W, int64_t ld, int32_t N, float *out,
                              hipStream_t s);
 

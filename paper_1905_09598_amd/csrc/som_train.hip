@@ -30,7 +30,9 @@
 // Per step the workgroup's (distance, unit) minimum goes to a grid exchange:
 // one 64-bit slot per workgroup and parity, dist_bits << 32 | tag << 24 |
 // unit, written and polled with relaxed device-scope atomics only (no fences,
-// so no cache write-back or invalidation).  The minimum over slots with the
+// so no cache write-back or invalidation).  The slot array is replicated once
+// per XCD and each workgroup polls its XCD's copy, which cuts the number of
+// pollers per cache line eightfold; slots are spread over cache lines.  The minimum over slots with the
 // current tag is the minimum over (distance, unit): squared distances are
 // non-negative, so their IEEE bits order like the values, and equal distances
 // fall to the lowest unit.  Slots alternate by step parity, so a fast
@@ -305,21 +307,25 @@ __device__ inline int exchange_wave0(const TrainArgs &a, int64_t e, unsigned lon
     const int lane = threadIdx.x & 63, G = a.grid;
     if (G == 1) return (int)(best & (unsigned long long)kMaxUnits);
     const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
-    unsigned long long *slots = a.slots + (e & 1) * (int64_t)G;
-    if (lane == 0) {
+    const int sp = a.slot_spread;
+    const int64_t par = (e & 1) * (int64_t)G * sp;
+    if (lane < kSlotReplicas) {
         const unsigned long long v = (best & 0xffffffff00000000ull) |
                                      ((unsigned long long)tag << kUnitBits) |
                                      (best & (unsigned long long)kMaxUnits);
-        __hip_atomic_store(slots + blockIdx.x, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(a.slots + lane * kSlotReplicaStride + par + (int64_t)blockIdx.x * sp,
+                           v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    const unsigned long long *slots =
+        a.slots + (blockIdx.x % kSlotReplicas) * kSlotReplicaStride + par;
     unsigned long long m = ~0ull;
     int abort = 0;
     for (int i = lane; i < G && !abort; i += 64) {
         const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
         unsigned spins = 0;
         for (;;) {
-            const unsigned long long v =
-                __hip_atomic_load(slots + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const unsigned long long v = __hip_atomic_load(slots + (int64_t)i * sp, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT);
             if (((unsigned)(v >> kUnitBits) & 0xffu) == tag) {
                 m = u64_min(m, v);
                 break;
@@ -380,6 +386,54 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
             for (int w = 1; w < WPR; ++w) v += part[idx * WPR + w];
             E[idx] = v;
         }
+    }
+    if (R <= 64) {
+        // Lane r keeps row r's Gram matrix and coefficients in registers.
+        float Er[T], gam[M], beta = 1.f;
+        float4 p = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int t = 0; t < T; ++t) Er[t] = lane < R ? E[lane * T + t] : 0.f;
+#pragma unroll
+        for (int j = 0; j < M; ++j) gam[j] = 0.f;
+        if (lane < R) p = pos[lane];
+        bool ok = true;
+#pragma unroll
+        for (int k = 0; k < M; ++k) {
+            if (k >= mb || !ok) continue;
+            const int64_t s = s0 + k;
+            const float2 sc = sw.get(a, s);
+            float lin = 0.f, quad = 0.f;
+#pragma unroll
+            for (int j = 0; j < k; ++j) {
+                float inner = 0.f;
+#pragma unroll
+                for (int i = 0; i < k; ++i) inner = fmaf(gam[i], Er[tri_any(i, j)], inner);
+                lin = fmaf(gam[j], Er[tri(j, k)], lin);
+                quad = fmaf(gam[j], inner, quad);
+            }
+            const float D = fmaf(-2.f, lin, Er[tri(k, k)]) + quad;
+            const unsigned long long best =
+                wave_min_u64(lane < R ? row_key(D, r0 + lane) : ~0ull);
+            const int c = exchange_wave0(a, s, best);
+            if (c < 0) {
+                ok = false;
+                continue;
+            }
+            const int cr = c / a.cols, ccol = c - cr * a.cols;
+            const float h = neighbour_h(a, p, (float)cr, (float)ccol, (float)(cr & 1), sc.x, sc.y);
+            const float om = 1.f - h;
+            beta *= om;
+#pragma unroll
+            for (int j = 0; j < k; ++j) gam[j] *= om;
+            gam[k] = h;
+            if (blockIdx.x == 0 && lane == 0 && a.bmu_trace) a.bmu_trace[s] = c;
+        }
+        if (lane < R) {
+            coef[lane * (M + 1)] = beta;
+#pragma unroll
+            for (int j = 0; j < M; ++j) coef[lane * (M + 1) + 1 + j] = gam[j];
+        }
+        return ok;
     }
     for (int r = lane; r < R; r += 64) {
         coef[r * (M + 1)] = 1.f;
@@ -564,9 +618,31 @@ size_t lds_bytes_for(const Instance &in, int rmax, bool ldsw) {
     return b;
 }
 
-// Estimated microseconds per step (model fitted to MI355X measurements of
-// the exchange and of LDS / memory sweeps); only ranks launch shapes.
-double exchange_us(int g) { return g <= 1 ? 0.2 : 0.6 + 0.3 * log2((double)g); }
+// Estimated microseconds per step, from MI355X measurements; only ranks
+// launch shapes.  Exchange latency by grid size (replicated, spread slots).
+double exchange_us(int g) {
+    static const double gs[] = {1, 8, 32, 64, 128, 256, 1024};
+    static const double us[] = {0.1, 1.1, 1.3, 1.35, 1.7, 2.5, 6.0};
+    if (g <= 1) return us[0];
+    for (int i = 1; i < 7; ++i)
+        if (g <= gs[i]) {
+            const double f = (log2((double)g) - log2(gs[i - 1])) / (log2(gs[i]) - log2(gs[i - 1]));
+            return us[i - 1] + f * (us[i] - us[i - 1]);
+        }
+    return us[6];
+}
+
+// Sweep time per step: VALU issue of the rows of one lane group (4 cycles
+// per wave64 instruction at 2.4 GHz) and, for streamed rows, memory traffic
+// at about 30 GB/s per CU; both spread over the block's M steps.
+double sweep_us(const Instance &in, int rmax, bool ldsw) {
+    const double P = 256.0 / in.lanes, M = in.m, T = M * (M + 1) / 2;
+    const double rows = ceil(rmax / P);
+    const double instr_per_row = in.k * (4 * M + 4 * T + 4 * (M + 1)) + 12 * T + 20;
+    const double valu = rows * instr_per_row * 4 / 2400.0;
+    const double mem = ldsw ? 0.0 : rmax * 2.0 * 16.0 * in.lanes * in.k / 30e3;
+    return (valu > mem ? valu : mem) / M + 1.0 / M;
+}
 
 }  // namespace
 
@@ -583,8 +659,6 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     hipError_t e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, 0);
     if (e != hipSuccess) return e;
     const int max_grid = a.N < num_cus ? a.N : num_cus;
-    // bytes moved per row per block sweep (read + write), spread over M steps
-    const double row_bytes = 2.0 * 16.0 * (double)ld4 / in->m;
 
     int grid = 0, variant = 0;
     if (a.grid > 0) {
@@ -593,32 +667,16 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
         variant = (a.variant != 2 && lds_bytes_for(*in, rmax, true) <= (size_t)max_lds) ? 1 : 0;
         if (a.variant == 1 && variant == 0) return hipErrorInvalidValue;
     } else {
-        // streamed sweep over the whole chip: about 30 GB/s per CU of memory
-        // traffic (measured at MALL-resident sizes) plus the exchange
-        double best;
-        {
-            const int g = max_grid;
-            const int rmax = (a.N + g - 1) / g;
-            best = exchange_us(g) + rmax * row_bytes / 30e3 + 0.5;
-            grid = g;
-            variant = 0;
-        }
-        if (a.variant != 2) {
-            // LDS-resident slices: ~300 GB/s of LDS traffic per CU
-            for (int g = 1; g <= max_grid; g *= 2) {
+        double best = 1e300;
+        for (int v = 0; v < 2; ++v) {
+            if ((v == 0 && a.variant == 1) || (v == 1 && a.variant == 2)) continue;
+            for (int g = 1;; g = g * 2 > max_grid && g < max_grid ? max_grid : g * 2) {
                 const int rmax = (a.N + g - 1) / g;
-                if (lds_bytes_for(*in, rmax, true) > (size_t)max_lds) continue;
-                const double t = exchange_us(g) + rmax * row_bytes / 300e3 + 0.3;
-                if (t < best) { best = t; grid = g; variant = 1; }
-            }
-            if (variant == 1) {
-                // a non-power-of-two grid up to the CU count may fit better
-                const int g = max_grid;
-                const int rmax = (a.N + g - 1) / g;
-                if (lds_bytes_for(*in, rmax, true) <= (size_t)max_lds) {
-                    const double t = exchange_us(g) + rmax * row_bytes / 300e3 + 0.3;
-                    if (t < best) { best = t; grid = g; }
+                if (v == 0 || lds_bytes_for(*in, rmax, true) <= (size_t)max_lds) {
+                    const double t = exchange_us(g) + sweep_us(*in, rmax, v == 1) + 0.3;
+                    if (t < best) { best = t; grid = g; variant = v; }
                 }
+                if (g >= max_grid) break;
             }
         }
     }
@@ -635,7 +693,11 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
                                                      kTrainBlock, lds);
     if (e != hipSuccess) return e;
     if (per_cu < 1 || grid > per_cu * num_cus) return hipErrorCooperativeLaunchTooLarge;
+    if (grid > kMaxTrainGrid) return hipErrorCooperativeLaunchTooLarge;
     plan->grid = grid;
+    // measured: one slot per 128-byte line is fastest up to 64 workgroups,
+    // 32-byte spacing beyond
+    plan->slot_spread = grid <= 64 ? 16 : 4;
     plan->block = kTrainBlock;
     plan->variant = variant;
     plan->kslots = in->k;
@@ -649,6 +711,7 @@ hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s
         return hipErrorInvalidValue;
     TrainArgs args = a;
     args.grid = plan.grid;
+    args.slot_spread = plan.slot_spread;
     TrainKernel fn = plan.variant ? in->lds : in->stream;
     void *params[] = {&args};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),

@@ -31,11 +31,17 @@ __global__ void init_uniform_kernel(float *W, int64_t ld, int32_t N, int32_t d,
     }
 }
 
-// Zero the exchange slots and the order flag (one workgroup).
-__global__ void reset_train_kernel(unsigned long long *slots, int32_t nslots,
+// Zero the exchange words a grid of `grid` workgroups uses (every replica,
+// both parities) and the order flag.
+__global__ void reset_train_kernel(unsigned long long *slots, int64_t per_replica,
                                    DevState *state) {
-    for (int i = threadIdx.x; i < nslots; i += blockDim.x) slots[i] = 0ull;
-    if (threadIdx.x == 0) state->order_bad = 0;
+    const int64_t total = kSlotReplicas * per_replica;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < total;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t rep = i / per_replica, off = i - rep * per_replica;
+        slots[rep * kSlotReplicaStride + off] = 0ull;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) state->order_bad = 0;
 }
 
 __device__ inline double decay_at(double a, double b, int kind, double p) {
@@ -101,9 +107,12 @@ hipError_t launch_init_uniform(float *W, int64_t ld, int32_t N, int32_t d,
     return hipGetLastError();
 }
 
-hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, int32_t nslots,
-                                hipStream_t s) {
-    reset_train_kernel<<<dim3(1), dim3(1024), 0, s>>>(a.slots, nslots, a.state);
+hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, hipStream_t s) {
+    if (a.grid < 1 || a.grid > kMaxTrainGrid || a.slot_spread < 1 ||
+        a.slot_spread > kMaxSlotSpread)
+        return hipErrorInvalidValue;
+    const int64_t per_replica = 2LL * a.grid * a.slot_spread;
+    reset_train_kernel<<<dim3(16), dim3(256), 0, s>>>(a.slots, per_replica, a.state);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t blocks = (a.nsteps + 255) / 256;
