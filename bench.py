@@ -174,7 +174,7 @@ def main():
             "train_steps_per_pass": cfg.steps,
             "schedule": f"lr {cfg.lr0}->{cfg.lr1} linear, sigma {cfg.sigma0}->{cfg.sigma1} exp",
             "grid": plan["grid"], "block": plan["block"],
-            "variant": ["stream", "lds"][plan["variant"]],
+            "variant": ["stream", "lds", "pipelined-stream", "pipelined-lds"][plan["variant"]],
         },
         "roofline": {
             "bound": "hbm",
@@ -183,7 +183,8 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
-            "kernel": f"train_kernel (variant {['stream', 'lds'][plan['variant']]})",
+            "kernel": ["train_kernel (stream)", "train_kernel (lds)",
+                       "train_pipe_kernel (stream)", "train_pipe_kernel (lds)"][plan["variant"]],
             "kernel_ms": avg_train_s * 1e3,
             "alg_bytes_per_launch": alg_bytes,
         },

@@ -176,9 +176,10 @@ som_status som_get_shape(const som_map *map, int32_t *rows, int32_t *cols,
 som_status som_shuffle(uint64_t seed, int64_t epoch, int64_t n, int32_t *out);
 
 /* Launch shape that som_train would use for this map: workgroups, threads
- * per workgroup and kernel variant (0 = prototypes streamed from memory each
- * step, 1 = prototypes held in LDS for the whole call).  Any output may be
- * NULL. */
+ * per workgroup and kernel variant (0 = prototypes streamed from memory once
+ * per block of steps, 1 = prototypes held in LDS for the whole call, 2 / 3 =
+ * the same with the pass over the prototypes overlapped with the grid
+ * exchanges).  Any output may be NULL. */
 som_status som_train_plan(const som_map *map, int32_t *grid, int32_t *block,
                           int32_t *variant);
 

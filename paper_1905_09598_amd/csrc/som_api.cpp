@@ -32,6 +32,9 @@ struct som_map {
     // per-step schedule table of the current training call
     float2 *sched = nullptr;
     int64_t sched_cap = 0;
+    // per-block sample products of the pipelined training kernel
+    float *block_dots = nullptr;
+    int64_t block_dots_cap = 0;
     // evaluation scratch
     float *wnorm = nullptr;
     int32_t *cand = nullptr, *idx1 = nullptr, *idx2 = nullptr;
@@ -266,6 +269,7 @@ som_status som_destroy(som_map *m) {
     if (m->order_host) (void)hipHostFree(m->order_host);
     if (m->order_done) (void)hipEventDestroy(m->order_done);
     (void)hipFree(m->sched);
+    (void)hipFree(m->block_dots);
     (void)hipFree(m->wnorm);
     (void)hipFree(m->cand);
     (void)hipFree(m->idx1);
@@ -318,9 +322,11 @@ static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
     a.grid = (g && *g) ? atoi(g) : 0;
     if (a.grid < 0) a.grid = 0;
     if (a.grid > som::kMaxTrainGrid) a.grid = som::kMaxTrainGrid;
+    // SOM_TRAIN_VARIANT: 1 LDS-resident, 2 streamed, 3 / 4 pipelined LDS /
+    // streamed, 5 never pipelined.
     const char *v = getenv("SOM_TRAIN_VARIANT");
     a.variant = (v && *v) ? atoi(v) : 0;
-    if (a.variant < 0 || a.variant > 2) a.variant = 0;
+    if (a.variant < 0 || a.variant > 5) a.variant = 0;
     a.timeout_ticks = 100000000ull * 20;  // 20 s at the 100 MHz reference clock
     return a;
 }
@@ -420,6 +426,20 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
         m->sched_cap = nsteps;
     }
     a.sched = m->sched;
+    if (plan.variant >= 2) {
+        const int64_t need = som::pipe_block_dots_floats(plan.pipe_m, nsteps);
+        if (m->block_dots_cap < need) {
+            e = hipStreamSynchronize(m->stream);
+            if (e == hipSuccess && m->block_dots) e = hipFree(m->block_dots);
+            m->block_dots = nullptr;
+            m->block_dots_cap = 0;
+            if (e == hipSuccess)
+                e = hipMalloc(reinterpret_cast<void **>(&m->block_dots), (size_t)need * sizeof(float));
+            if (e != hipSuccess) return from_hip(e);
+            m->block_dots_cap = need;
+        }
+        a.block_dots = m->block_dots;
+    }
     a.grid = plan.grid;
     a.slot_spread = plan.slot_spread;
     e = som::launch_prepare_train(a, m->sched, m->stream);

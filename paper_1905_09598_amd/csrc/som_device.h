@@ -1,0 +1,345 @@
+// Device helpers shared by the training kernels: wave reductions, per-step
+// input windows, sample loads, the grid exchange and the neighbourhood
+// factor.  Included by the kernel translation units only.
+#pragma once
+
+#include "som_internal.h"
+
+#include <math.h>
+
+namespace som {
+namespace dev {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int32_t kStatusTimeout = 5;  // SOM_E_TIMEOUT
+
+// Prototype rows live either in LDS or in global memory.  Pointers typed
+// with the address space make the compiler use LDS (ds_*) or global
+// instructions instead of generic (flat) ones, which count against both
+// memory counters and so make every wait for a row also wait for any
+// outstanding sample load.
+template <bool LDS>
+struct RowSpace {
+    typedef __attribute__((address_space(1))) f4 T;
+};
+template <>
+struct RowSpace<true> {
+    typedef __attribute__((address_space(3))) f4 T;
+};
+template <bool LDS>
+using row_t = typename RowSpace<LDS>::T;
+template <bool LDS>
+__device__ inline row_t<LDS> *rows_as(f4 *p) {
+    return (row_t<LDS> *)p;
+}
+
+// Sums over the 64 lanes of a wave, for U values at once, returned to every
+// lane.  Within each row of 16 lanes a butterfly of DPP moves (quad swaps,
+// half-row and row mirrors) leaves the row's sum in all of its lanes,
+// bit-identical because every pairwise add is commutative; the four row sums
+// are then read out and added in a fixed order.  The U chains run in
+// lockstep so their DPP hazards overlap.
+template <int CTRL>
+__device__ inline int dpp_move(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
+}
+template <int CTRL>
+__device__ inline float dpp_pair(float v) {
+    return v + __int_as_float(dpp_move<CTRL>(__float_as_int(v)));
+}
+__device__ inline float lane_f(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+template <int U>
+__device__ inline void wave_sums(float (&v)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0xB1>(v[u]);   // quad_perm [1,0,3,2]
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x4E>(v[u]);   // quad_perm [2,3,0,1]
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x141>(v[u]);  // row_half_mirror
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x140>(v[u]);  // row_mirror
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+        v[u] = (lane_f(v[u], 0) + lane_f(v[u], 16)) + (lane_f(v[u], 32) + lane_f(v[u], 48));
+}
+
+__device__ inline unsigned long long u64_min(unsigned long long a, unsigned long long b) {
+    return a < b ? a : b;
+}
+
+// Minimum over the 64 lanes of a wave (same DPP pattern), to every lane.
+__device__ inline unsigned wave_min_u32(unsigned v) {
+    v = min(v, (unsigned)dpp_move<0xB1>((int)v));
+    v = min(v, (unsigned)dpp_move<0x4E>((int)v));
+    v = min(v, (unsigned)dpp_move<0x141>((int)v));
+    v = min(v, (unsigned)dpp_move<0x140>((int)v));
+    const unsigned a = (unsigned)__builtin_amdgcn_readlane((int)v, 0);
+    const unsigned b = (unsigned)__builtin_amdgcn_readlane((int)v, 16);
+    const unsigned c = (unsigned)__builtin_amdgcn_readlane((int)v, 32);
+    const unsigned d = (unsigned)__builtin_amdgcn_readlane((int)v, 48);
+    return min(min(a, b), min(c, d));
+}
+
+// Minimum of a 64-bit key over the wave: the high words first, then the low
+// words among the lanes that hold the minimal high word (usually one).
+__device__ inline unsigned long long wave_min_key(unsigned long long v) {
+    const unsigned hi = (unsigned)(v >> 32), lo = (unsigned)v;
+    const unsigned mh = wave_min_u32(hi);
+    const unsigned long long hit = __ballot(hi == mh);
+    unsigned ml;
+    if (__builtin_popcountll(hit) == 1)
+        ml = (unsigned)__builtin_amdgcn_readlane((int)lo, __builtin_ctzll(hit));
+    else
+        ml = wave_min_u32(hi == mh ? lo : 0xffffffffu);
+    return ((unsigned long long)mh << 32) | ml;
+}
+
+// Distance bits that compare as unsigned integers in the order of the
+// distances: NaN counts as +inf, -0 as +0, and a negative value (the
+// rounding of a near-zero distance in Gram form) below every positive one.
+__device__ inline unsigned dist_order_bits(float D) {
+    const unsigned b = __float_as_uint(fminf(D, INFINITY) + 0.f);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+// Key (distance bits << 32 | unit) of the smallest of the lanes' distance
+// bits, ties to the lowest lane; lane l stands for unit u0 + l.  Idle lanes
+// pass 0xffffffff, which no distance maps to; lane 0 must not be idle.
+__device__ inline unsigned long long wave_argmin_key(unsigned bits, int u0) {
+    const unsigned m = wave_min_u32(bits);
+    const unsigned long long hit = __ballot(bits == m);
+    return ((unsigned long long)m << 32) | (unsigned)(u0 + __builtin_ctzll(hit));
+}
+
+// Sample row i into the lane's slots; columns past d (row padding) are 0.
+template <int K, int L>
+__device__ inline void load_sample(f4 (&x)[K], const TrainArgs &a, int64_t i) {
+    const int li = threadIdx.x % L;
+    if (a.x_vec4) {
+        const f4 *xr = reinterpret_cast<const f4 *>(a.X + i * a.d);
+        const int xd4 = a.d >> 2;  // d % 4 == 0 on this path
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const int q = li + L * k;
+            x[k] = (q < xd4) ? xr[q] : f4{0.f, 0.f, 0.f, 0.f};
+        }
+    } else {
+        const float *xr = a.X + i * a.d;
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const int j = 4 * (li + L * k);
+            f4 v;
+            v.x = (j + 0 < a.d) ? xr[j + 0] : 0.f;
+            v.y = (j + 1 < a.d) ? xr[j + 1] : 0.f;
+            v.z = (j + 2 < a.d) ? xr[j + 2] : 0.f;
+            v.w = (j + 3 < a.d) ? xr[j + 3] : 0.f;
+            x[k] = v;
+        }
+    }
+}
+
+// Per-step inputs (sample index, schedule entry) are fetched 64 steps at a
+// time: lane l of a window holds the entry of step base + l, loaded with one
+// vector load, and a step's entry is read out with readlane.  Vector loads
+// keep these fetches off the scalar-memory counter that LDS operations
+// share, so waiting for LDS never waits for them.  The next window is
+// loaded while the current one is in use.
+__device__ inline int fetch_entry(const TrainArgs &a, int64_t s, int) {
+    int i = s < a.nsteps ? a.order[s] : 0;
+    return (i >= 0 && (int64_t)i < a.n) ? i : 0;  // range-checked before launch
+}
+__device__ inline float2 fetch_entry(const TrainArgs &a, int64_t s, float2) {
+    return s < a.nsteps ? a.sched[s] : make_float2(0.f, 0.f);
+}
+
+template <typename T>
+struct StepWindow {
+    int64_t base;
+    T cur, next;
+
+    __device__ void init(const TrainArgs &a, int64_t b) {
+        base = b;
+        cur = fetch_entry(a, b + (threadIdx.x & 63), T());
+        next = fetch_entry(a, b + 64 + (threadIdx.x & 63), T());
+    }
+    // Entry of step s, for non-decreasing s >= base.
+    __device__ T get(const TrainArgs &a, int64_t s) {
+        if (s >= base + 64) {
+            base += 64;
+            cur = next;
+            next = fetch_entry(a, base + 64 + (threadIdx.x & 63), T());
+        }
+        return lane_value((int)(s - base));
+    }
+    __device__ T lane_value(int l) const;
+};
+
+template <>
+__device__ inline int StepWindow<int>::lane_value(int l) const {
+    return __builtin_amdgcn_readlane(cur, l);
+}
+template <>
+__device__ inline float2 StepWindow<float2>::lane_value(int l) const {
+    return make_float2(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(cur.x), l)),
+                       __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cur.y), l)));
+}
+
+
+// Packed index of the Gram entry (i, j), i <= j.
+__device__ constexpr int tri(int i, int j) { return j * (j + 1) / 2 + i; }
+__device__ constexpr int tri_any(int i, int j) { return i <= j ? tri(i, j) : tri(j, i); }
+
+__device__ inline unsigned long long row_key(float D, int u) {
+    return ((unsigned long long)dist_order_bits(D) << 32) | (unsigned)u;
+}
+
+// Lattice row and column of unit c < 2^24: the fp32 quotient c * (1 / cols)
+// is within one of c / cols (both roundings are exact for cols <= 2 and
+// the error stays below 2^24 / cols * 2^-23 < 1 otherwise), so one
+// correction step makes it exact.
+__device__ inline void unit_rc(int c, int cols, float inv_cols, int &r, int &col) {
+    int q = (int)((float)c * inv_cols);
+    int rem = c - q * cols;
+    if (rem < 0) {
+        --q;
+        rem += cols;
+    } else if (rem >= cols) {
+        ++q;
+        rem -= cols;
+    }
+    r = q;
+    col = rem;
+}
+
+struct Bcast {
+    int abort;
+    int pad[3];
+};
+
+// One wave per workgroup: publish this workgroup's best key to grid
+// exchange number e and return the winning unit over every workgroup's slot
+// (the same in all lanes), or -1 if the wait was given up.
+__device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long best) {
+    const int lane = threadIdx.x & 63, G = a.grid;
+    if (G == 1) return (int)(best & (unsigned long long)kMaxUnits);
+    const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
+    const int sp = a.slot_spread;
+    const int64_t par = (e & 1) * (int64_t)G * sp;
+    if (lane < kSlotReplicas) {
+        const unsigned long long v = (best & 0xffffffff00000000ull) |
+                                     ((unsigned long long)tag << kUnitBits) |
+                                     (best & (unsigned long long)kMaxUnits);
+        __hip_atomic_store(a.slots + lane * kSlotReplicaStride + par + (int64_t)blockIdx.x * sp,
+                           v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    const unsigned long long *slots =
+        a.slots + (blockIdx.x % kSlotReplicas) * kSlotReplicaStride + par;
+    unsigned long long m = ~0ull;
+    int abort = 0;
+    for (int i = lane; i < G && !abort; i += 64) {
+        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+        unsigned spins = 0;
+        for (;;) {
+            const unsigned long long v = __hip_atomic_load(slots + (int64_t)i * sp, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT);
+            if (((unsigned)(v >> kUnitBits) & 0xffu) == tag) {
+                m = u64_min(m, v);
+                break;
+            }
+            if ((++spins & 63u) == 0) {
+                if (__hip_atomic_load(&a.state->status, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT) != 0) {
+                    abort = 1;
+                    break;
+                }
+                if (__builtin_amdgcn_s_memrealtime() - t0 > a.timeout_ticks) {
+                    __hip_atomic_store(&a.state->status, kStatusTimeout, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+                    abort = 1;
+                    break;
+                }
+            }
+        }
+    }
+    m = wave_min_key(m);
+    if (__ballot(abort) != 0) return -1;
+    return (int)(m & (unsigned long long)kMaxUnits);
+}
+
+// Neighbourhood factor of owned row r given BMU c: lr * 2^(-g * c2) with g
+// the squared lattice distance.  pos[r] holds (row, column, row parity) of
+// unit r0 + r.  RECT: g = dr^2 + dc^2.  HEX: odd rows shifted by 1/2 and rows
+// sqrt(3)/2 apart, so g = 3/4 dr^2 + (dc + (parity difference) / 2)^2, exact
+// in fp32 for the map sizes the library accepts.
+__device__ inline float neighbour_h(const TrainArgs &a, float4 p, float cr, float cc,
+                                    float cpar, float lr, float c2) {
+    const float dr = p.x - cr;
+    float dx = p.y - cc, g;
+    if (a.topology == 1) {
+        dx += 0.5f * (p.z - cpar);
+        g = 0.75f * dr * dr + dx * dx;
+    } else {
+        g = dr * dr + dx * dx;
+    }
+    return lr * exp2f(-g * c2);
+}
+
+// One wave per workgroup runs the mb steps s0 .. s0 + mb - 1 of a block from
+// the Gram matrices E of the workgroup's rows (lane r holds row r < R, with
+// lattice position p), leaving the block's coefficients in (beta, gam):
+// after the block a prototype is w_end = beta w_start + sum_j gam_j x_j.
+// Step k's distance D_k = E_kk - 2 sum_j gam_j E_jk + sum_ij gam_i gam_j E_ij
+// is carried from step to step through lin_l = sum_j gam_j E_jl and
+// quad = sum_ij gam_i gam_j E_ij: a step with factor h scales every gam by
+// (1 - h) and sets gam_k = h, so
+//   quad <- (1 - h)^2 quad + 2 h (1 - h) lin_k + h^2 E_kk,
+//   lin_l <- (1 - h) lin_l + h E_kl.
+// Returns false if an exchange was given up.
+template <int M>
+__device__ inline bool block_steps(const TrainArgs &a, int64_t s0, int mb, int r0, int R,
+                                   const float (&E)[M * (M + 1) / 2], float4 p, float inv_cols,
+                                   StepWindow<float2> &sw, float &beta, float (&gam)[M]) {
+    const int lane = threadIdx.x & 63;
+    float lin[M], quad = 0.f;
+    beta = 1.f;
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+        gam[j] = 0.f;
+        lin[j] = 0.f;
+    }
+    bool ok = true;
+#pragma unroll
+    for (int k = 0; k < M; ++k) {
+        if (k >= mb || !ok) continue;
+        const int64_t s = s0 + k;
+        const float2 sc = sw.get(a, s);
+        const float Ekk = E[tri(k, k)];
+        const float D = fmaf(-2.f, lin[k], Ekk) + quad;
+        const unsigned long long best =
+            wave_argmin_key(lane < R ? dist_order_bits(D) : 0xffffffffu, r0);
+        const int c = exchange(a, s, best);
+        if (c < 0) {
+            ok = false;
+            continue;
+        }
+        int cr, cc;
+        unit_rc(c, a.cols, inv_cols, cr, cc);
+        const float h = neighbour_h(a, p, (float)cr, (float)cc, (float)(cr & 1), sc.x, sc.y);
+        const float om = 1.f - h;
+        quad = fmaf(om * om, quad, h * fmaf(2.f * om, lin[k], h * Ekk));
+#pragma unroll
+        for (int l = k + 1; l < M; ++l) lin[l] = fmaf(h, E[tri(k, l)], om * lin[l]);
+        beta *= om;
+#pragma unroll
+        for (int j = 0; j < k; ++j) gam[j] *= om;
+        gam[k] = h;
+        if (blockIdx.x == 0 && lane == 0 && a.bmu_trace) a.bmu_trace[s] = c;
+    }
+    return ok;
+}
+
+}  // namespace dev
+}  // namespace som

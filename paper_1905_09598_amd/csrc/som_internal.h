@@ -39,6 +39,7 @@ struct TrainArgs {
     double lr0, lr1, sigma0, sigma1;
     int32_t lr_decay, sigma_decay;
     const float2 *sched;    // nsteps (lr, log2(e) / (2 sigma^2)) of the call's steps
+    float *block_dots;      // pipelined variant: per-block sample products
     int32_t *bmu_trace;     // nullable, nsteps entries
     unsigned long long *slots;  // kSlotWords exchange words
     int32_t slot_spread;        // u64 between consecutive workgroups' slots
@@ -52,7 +53,8 @@ struct TrainArgs {
 struct TrainPlan {
     int32_t grid = 0;
     int32_t block = kTrainBlock;
-    int32_t variant = 0;     // 0 = streamed prototypes, 1 = LDS-resident
+    int32_t variant = 0;     // 0 streamed, 1 LDS-resident, 2 / 3 pipelined streamed / LDS
+    int32_t pipe_m = 0;      // block length of the pipelined variants
     int32_t kslots = 0;      // float4 columns per lane (template instance)
     int32_t slot_spread = 1;
     size_t lds_bytes = 0;
@@ -78,6 +80,13 @@ __device__ inline double lattice_sq(int u, int c, int cols, int topology) {
 // kernel's lane slots (16-byte columns times lanes per row), so the sweep
 // needs no column bounds; 0 when no training kernel covers d.
 int64_t train_row_pitch(int32_t d);
+
+// Pipelined training (som_train_pipe.hip): estimated microseconds per step
+// of its best shape (1e300 if none fits), written into *plan.
+double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *plan,
+                       double (*exchange_us)(int));
+int64_t pipe_block_dots_floats(int m, int64_t nsteps);
+hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStream_t s);
 
 // Host-side launchers (each translation unit owns its kernels).
 hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan);

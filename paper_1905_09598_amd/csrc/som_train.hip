@@ -39,158 +39,14 @@
 // workgroup can publish step e+1 while a slow one still reads step e.  Every
 // wait is bounded in time and also ends when any workgroup has flagged an
 // error.
-#include "som_internal.h"
-
-#include <math.h>
+#include "som_device.h"
 
 namespace som {
 namespace {
 
-typedef float f4 __attribute__((ext_vector_type(4)));
+using namespace dev;
 
-constexpr int32_t kStatusTimeout = 5;  // SOM_E_TIMEOUT
-constexpr int kHeader = 64;            // LDS bytes for the broadcast words
-
-// Sums over the 64 lanes of a wave, for U values at once, returned to every
-// lane.  Within each row of 16 lanes a butterfly of DPP moves (quad swaps,
-// half-row and row mirrors) leaves the row's sum in all of its lanes,
-// bit-identical because every pairwise add is commutative; the four row sums
-// are then read out and added in a fixed order.  The U chains run in
-// lockstep so their DPP hazards overlap.
-template <int CTRL>
-__device__ inline int dpp_move(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xf, 0xf, false);
-}
-template <int CTRL>
-__device__ inline float dpp_pair(float v) {
-    return v + __int_as_float(dpp_move<CTRL>(__float_as_int(v)));
-}
-__device__ inline float lane_f(float v, int l) {
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
-}
-template <int U>
-__device__ inline void wave_sums(float (&v)[U]) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0xB1>(v[u]);   // quad_perm [1,0,3,2]
-#pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x4E>(v[u]);   // quad_perm [2,3,0,1]
-#pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x141>(v[u]);  // row_half_mirror
-#pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x140>(v[u]);  // row_mirror
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-        v[u] = (lane_f(v[u], 0) + lane_f(v[u], 16)) + (lane_f(v[u], 32) + lane_f(v[u], 48));
-}
-
-__device__ inline unsigned long long u64_min(unsigned long long a, unsigned long long b) {
-    return a < b ? a : b;
-}
-
-template <int CTRL>
-__device__ inline unsigned long long dpp_min_u64(unsigned long long v) {
-    const unsigned lo = (unsigned)dpp_move<CTRL>((int)(unsigned)(v & 0xffffffffu));
-    const unsigned hi = (unsigned)dpp_move<CTRL>((int)(unsigned)(v >> 32));
-    return u64_min(v, ((unsigned long long)hi << 32) | lo);
-}
-
-__device__ inline unsigned long long lane_u64(unsigned long long v, int l) {
-    const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(v & 0xffffffffu), l);
-    const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(v >> 32), l);
-    return ((unsigned long long)hi << 32) | lo;
-}
-
-// Minimum over the 64 lanes of a wave (same DPP pattern), to every lane.
-__device__ inline unsigned long long wave_min_u64(unsigned long long v) {
-    v = dpp_min_u64<0xB1>(v);
-    v = dpp_min_u64<0x4E>(v);
-    v = dpp_min_u64<0x141>(v);
-    v = dpp_min_u64<0x140>(v);
-    return u64_min(u64_min(lane_u64(v, 0), lane_u64(v, 16)),
-                   u64_min(lane_u64(v, 32), lane_u64(v, 48)));
-}
-
-// Sample row i into the lane's slots; columns past d (row padding) are 0.
-template <int K, int L>
-__device__ inline void load_sample(f4 (&x)[K], const TrainArgs &a, int64_t i) {
-    const int li = threadIdx.x % L;
-    if (a.x_vec4) {
-        const f4 *xr = reinterpret_cast<const f4 *>(a.X + i * a.d);
-        const int xd4 = a.d >> 2;  // d % 4 == 0 on this path
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const int q = li + L * k;
-            x[k] = (q < xd4) ? xr[q] : f4{0.f, 0.f, 0.f, 0.f};
-        }
-    } else {
-        const float *xr = a.X + i * a.d;
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const int j = 4 * (li + L * k);
-            f4 v;
-            v.x = (j + 0 < a.d) ? xr[j + 0] : 0.f;
-            v.y = (j + 1 < a.d) ? xr[j + 1] : 0.f;
-            v.z = (j + 2 < a.d) ? xr[j + 2] : 0.f;
-            v.w = (j + 3 < a.d) ? xr[j + 3] : 0.f;
-            x[k] = v;
-        }
-    }
-}
-
-// Per-step inputs (sample index, schedule entry) are fetched 64 steps at a
-// time: lane l of a window holds the entry of step base + l, loaded with one
-// vector load, and a step's entry is read out with readlane.  Vector loads
-// keep these fetches off the scalar-memory counter that LDS operations
-// share, so waiting for LDS never waits for them.  The next window is
-// loaded while the current one is in use.
-__device__ inline int fetch_entry(const TrainArgs &a, int64_t s, int) {
-    int i = s < a.nsteps ? a.order[s] : 0;
-    return (i >= 0 && (int64_t)i < a.n) ? i : 0;  // range-checked before launch
-}
-__device__ inline float2 fetch_entry(const TrainArgs &a, int64_t s, float2) {
-    return s < a.nsteps ? a.sched[s] : make_float2(0.f, 0.f);
-}
-
-template <typename T>
-struct StepWindow {
-    int64_t base;
-    T cur, next;
-
-    __device__ void init(const TrainArgs &a, int64_t b) {
-        base = b;
-        cur = fetch_entry(a, b + (threadIdx.x & 63), T());
-        next = fetch_entry(a, b + 64 + (threadIdx.x & 63), T());
-    }
-    // Entry of step s, for non-decreasing s >= base.
-    __device__ T get(const TrainArgs &a, int64_t s) {
-        if (s >= base + 64) {
-            base += 64;
-            cur = next;
-            next = fetch_entry(a, base + 64 + (threadIdx.x & 63), T());
-        }
-        return lane_value((int)(s - base));
-    }
-    __device__ T lane_value(int l) const;
-};
-
-template <>
-__device__ inline int StepWindow<int>::lane_value(int l) const {
-    return __builtin_amdgcn_readlane(cur, l);
-}
-template <>
-__device__ inline float2 StepWindow<float2>::lane_value(int l) const {
-    return make_float2(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(cur.x), l)),
-                       __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cur.y), l)));
-}
-
-
-// Packed index of the Gram entry (i, j), i <= j.
-__device__ constexpr int tri(int i, int j) { return j * (j + 1) / 2 + i; }
-__device__ constexpr int tri_any(int i, int j) { return i <= j ? tri(i, j) : tri(j, i); }
-
-__device__ inline unsigned long long row_key(float D, int u) {
-    return ((unsigned long long)__float_as_uint(D) << 32) | (unsigned)u;
-}
+constexpr int kHeader = 64;  // LDS bytes for the broadcast words
 
 // Lane layout.  A workgroup's 256 threads form P = 256 / L groups of L
 // lanes; group g sweeps rows g, g + P, g + 2P, ... of the workgroup's slice,
@@ -215,9 +71,10 @@ __device__ inline void load_block(f4 (&x)[M][K], const TrainArgs &a, int64_t s_b
 // from coef[r] = (beta, gamma_0..gamma_{M-1}); GRAM accumulates the Gram
 // matrix of e_j = xg_j - w over the (updated) row into E[r] (or, with more
 // than one wave per row, the wave's partials into part[(r * T + t) * WPR + w]).
-template <int K, int L, int M, int U, bool UPD, bool GRAM>
-__device__ inline void sweep(f4 *__restrict__ rows, int R, const f4 (&xu)[M][K],
-                             const f4 (&xg)[M][K], const float *coef, float *E, float *part) {
+template <int K, int L, int M, int U, bool LDSW, bool UPD, bool GRAM>
+__device__ inline void sweep(f4 *rows_p, int R, const f4 (&xu)[M][K], const f4 (&xg)[M][K],
+                             const float *coef, float *E, float *part) {
+    row_t<LDSW> *__restrict__ rows = rows_as<LDSW>(rows_p);
     constexpr int P = kTrainBlock / L;
     constexpr int P4 = L * K;
     constexpr int T = M * (M + 1) / 2;
@@ -229,7 +86,7 @@ __device__ inline void sweep(f4 *__restrict__ rows, int R, const f4 (&xu)[M][K],
         for (int u = 0; u < U; ++u) {
             const int r = rb + u * P;
             if (r < R) {
-                const f4 *row = rows + (size_t)r * P4 + li;
+                const row_t<LDSW> *row = rows + (size_t)r * P4 + li;
 #pragma unroll
                 for (int k = 0; k < K; ++k) w[u][k] = row[L * k];
             }
@@ -238,7 +95,7 @@ __device__ inline void sweep(f4 *__restrict__ rows, int R, const f4 (&xu)[M][K],
         for (int u = 0; u < U; ++u) {
             const int r = rb + u * P;
             if (r >= R) continue;
-            f4 *row = rows + (size_t)r * P4 + li;
+            row_t<LDSW> *row = rows + (size_t)r * P4 + li;
             float beta = 1.f, gam[M];
 #pragma unroll
             for (int j = 0; j < M; ++j) gam[j] = 0.f;
@@ -295,79 +152,6 @@ __device__ inline void sweep(f4 *__restrict__ rows, int R, const f4 (&xu)[M][K],
     }
 }
 
-struct Bcast {
-    int abort;
-    int pad[3];
-};
-
-// Wave 0 only: publish this workgroup's best key to grid exchange number e
-// and return the winning unit over every workgroup's slot (the same in all
-// lanes), or -1 if the wait was given up.
-__device__ inline int exchange_wave0(const TrainArgs &a, int64_t e, unsigned long long best) {
-    const int lane = threadIdx.x & 63, G = a.grid;
-    if (G == 1) return (int)(best & (unsigned long long)kMaxUnits);
-    const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
-    const int sp = a.slot_spread;
-    const int64_t par = (e & 1) * (int64_t)G * sp;
-    if (lane < kSlotReplicas) {
-        const unsigned long long v = (best & 0xffffffff00000000ull) |
-                                     ((unsigned long long)tag << kUnitBits) |
-                                     (best & (unsigned long long)kMaxUnits);
-        __hip_atomic_store(a.slots + lane * kSlotReplicaStride + par + (int64_t)blockIdx.x * sp,
-                           v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    const unsigned long long *slots =
-        a.slots + (blockIdx.x % kSlotReplicas) * kSlotReplicaStride + par;
-    unsigned long long m = ~0ull;
-    int abort = 0;
-    for (int i = lane; i < G && !abort; i += 64) {
-        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-        unsigned spins = 0;
-        for (;;) {
-            const unsigned long long v = __hip_atomic_load(slots + (int64_t)i * sp, __ATOMIC_RELAXED,
-                                                           __HIP_MEMORY_SCOPE_AGENT);
-            if (((unsigned)(v >> kUnitBits) & 0xffu) == tag) {
-                m = u64_min(m, v);
-                break;
-            }
-            if ((++spins & 63u) == 0) {
-                if (__hip_atomic_load(&a.state->status, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT) != 0) {
-                    abort = 1;
-                    break;
-                }
-                if (__builtin_amdgcn_s_memrealtime() - t0 > a.timeout_ticks) {
-                    __hip_atomic_store(&a.state->status, kStatusTimeout, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-                    abort = 1;
-                    break;
-                }
-            }
-        }
-    }
-    m = wave_min_u64(m);
-    if (__ballot(abort) != 0) return -1;
-    return (int)(m & (unsigned long long)kMaxUnits);
-}
-
-// Neighbourhood factor of owned row r given BMU c: lr * 2^(-g * c2) with g
-// the squared lattice distance.  pos[r] holds (row, column, row parity) of
-// unit r0 + r.  RECT: g = dr^2 + dc^2.  HEX: odd rows shifted by 1/2 and rows
-// sqrt(3)/2 apart, so g = 3/4 dr^2 + (dc + (parity difference) / 2)^2, exact
-// in fp32 for the map sizes the library accepts.
-__device__ inline float neighbour_h(const TrainArgs &a, float4 p, float cr, float cc,
-                                    float cpar, float lr, float c2) {
-    const float dr = p.x - cr;
-    float dx = p.y - cc, g;
-    if (a.topology == 1) {
-        dx += 0.5f * (p.z - cpar);
-        g = 0.75f * dr * dr + dx * dx;
-    } else {
-        g = dr * dr + dx * dx;
-    }
-    return lr * exp2f(-g * c2);
-}
-
 // Wave 0 only: the BMUs of the block's mb steps, s0 .. s0 + mb - 1, from the
 // Gram matrices E of the owned rows (LDS), leaving each row's update
 // coefficients (beta, gamma_0..) in coef.  Returns false if an exchange
@@ -379,6 +163,7 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
     constexpr int T = M * (M + 1) / 2;
     constexpr int WPR = L / 64;
     const int lane = threadIdx.x & 63;
+    const float inv_cols = 1.f / (float)a.cols;
     if (WPR > 1) {
         for (int idx = lane; idx < R * T; idx += 64) {
             float v = part[idx * WPR];
@@ -389,45 +174,12 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
     }
     if (R <= 64) {
         // Lane r keeps row r's Gram matrix and coefficients in registers.
-        float Er[T], gam[M], beta = 1.f;
+        float Er[T], gam[M], beta;
         float4 p = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int t = 0; t < T; ++t) Er[t] = lane < R ? E[lane * T + t] : 0.f;
-#pragma unroll
-        for (int j = 0; j < M; ++j) gam[j] = 0.f;
         if (lane < R) p = pos[lane];
-        bool ok = true;
-#pragma unroll
-        for (int k = 0; k < M; ++k) {
-            if (k >= mb || !ok) continue;
-            const int64_t s = s0 + k;
-            const float2 sc = sw.get(a, s);
-            float lin = 0.f, quad = 0.f;
-#pragma unroll
-            for (int j = 0; j < k; ++j) {
-                float inner = 0.f;
-#pragma unroll
-                for (int i = 0; i < k; ++i) inner = fmaf(gam[i], Er[tri_any(i, j)], inner);
-                lin = fmaf(gam[j], Er[tri(j, k)], lin);
-                quad = fmaf(gam[j], inner, quad);
-            }
-            const float D = fmaf(-2.f, lin, Er[tri(k, k)]) + quad;
-            const unsigned long long best =
-                wave_min_u64(lane < R ? row_key(D, r0 + lane) : ~0ull);
-            const int c = exchange_wave0(a, s, best);
-            if (c < 0) {
-                ok = false;
-                continue;
-            }
-            const int cr = c / a.cols, ccol = c - cr * a.cols;
-            const float h = neighbour_h(a, p, (float)cr, (float)ccol, (float)(cr & 1), sc.x, sc.y);
-            const float om = 1.f - h;
-            beta *= om;
-#pragma unroll
-            for (int j = 0; j < k; ++j) gam[j] *= om;
-            gam[k] = h;
-            if (blockIdx.x == 0 && lane == 0 && a.bmu_trace) a.bmu_trace[s] = c;
-        }
+        const bool ok = block_steps<M>(a, s0, mb, r0, R, Er, p, inv_cols, sw, beta, gam);
         if (lane < R) {
             coef[lane * (M + 1)] = beta;
 #pragma unroll
@@ -460,12 +212,13 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
             const float D = fmaf(-2.f, lin, Er[tri(k, k)]) + quad;
             best = u64_min(best, row_key(D, r0 + r));
         }
-        best = wave_min_u64(best);
-        const int c = exchange_wave0(a, s, best);
+        best = wave_min_key(best);
+        const int c = exchange(a, s, best);
         if (c < 0) return false;
         if (blockIdx.x == 0 && lane == 0 && a.bmu_trace) a.bmu_trace[s] = c;
         const float2 sc = sw.get(a, s);
-        const int cr = c / a.cols, ccol = c - cr * a.cols;
+        int cr, ccol;
+        unit_rc(c, a.cols, inv_cols, cr, ccol);
         const float fcr = (float)cr, fcc = (float)ccol, fcp = (float)(cr & 1);
         for (int r = lane; r < R; r += 64) {
             const float h = neighbour_h(a, pos[r], fcr, fcc, fcp, sc.x, sc.y);
@@ -510,7 +263,7 @@ __device__ inline Layout layout(unsigned char *smem, int R) {
 // One block: its BMUs (wave 0), then one sweep that applies the block's
 // updates with samples xu and accumulates the next block's Gram matrices
 // with samples xg, then the samples of the block after next go into xu.
-template <int K, int L, int M, int U>
+template <int K, int L, int M, int U, bool LDSW>
 __device__ inline bool run_block(const TrainArgs &a, int64_t blk, int64_t nblocks, int r0,
                                  int R, f4 *rows, const Layout &l, f4 (&xu)[M][K],
                                  const f4 (&xg)[M][K], StepWindow<int> &ow,
@@ -525,9 +278,9 @@ __device__ inline bool run_block(const TrainArgs &a, int64_t blk, int64_t nblock
     __syncthreads();
     if (bc->abort) return false;
     if (blk + 1 < nblocks)
-        sweep<K, L, M, U, true, true>(rows, R, xu, xg, l.coef, l.E, l.part);
+        sweep<K, L, M, U, LDSW, true, true>(rows, R, xu, xg, l.coef, l.E, l.part);
     else
-        sweep<K, L, M, U, true, false>(rows, R, xu, xg, l.coef, l.E, l.part);
+        sweep<K, L, M, U, LDSW, true, false>(rows, R, xu, xg, l.coef, l.E, l.part);
     if (blk + 2 < nblocks) load_block<K, L, M>(xu, a, (blk + 2) * M, ow);
     __syncthreads();
     return true;
@@ -568,13 +321,13 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
     if (nblocks > 1) load_block<K, L, M>(xB, a, M, ow);
     __syncthreads();
     // Gram matrices of block 0 against the initial prototypes.
-    sweep<K, L, M, U, false, true>(rows, R, xA, xA, l.coef, l.E, l.part);
+    sweep<K, L, M, U, LDSW, false, true>(rows, R, xA, xA, l.coef, l.E, l.part);
     __syncthreads();
 
     for (int64_t blk = 0; blk < nblocks; blk += 2) {
-        if (!run_block<K, L, M, U>(a, blk, nblocks, r0, R, rows, l, xA, xB, ow, sw, bc)) return;
+        if (!run_block<K, L, M, U, LDSW>(a, blk, nblocks, r0, R, rows, l, xA, xB, ow, sw, bc)) return;
         if (blk + 1 < nblocks &&
-            !run_block<K, L, M, U>(a, blk + 1, nblocks, r0, R, rows, l, xB, xA, ow, sw, bc))
+            !run_block<K, L, M, U, LDSW>(a, blk + 1, nblocks, r0, R, rows, l, xB, xA, ow, sw, bc))
             return;
     }
     if (LDSW)
@@ -620,7 +373,7 @@ size_t lds_bytes_for(const Instance &in, int rmax, bool ldsw) {
 
 // Estimated microseconds per step, from MI355X measurements; only ranks
 // launch shapes.  Exchange latency by grid size (replicated, spread slots).
-double exchange_us(int g) {
+double exchange_us_impl(int g) {
     static const double gs[] = {1, 8, 32, 64, 128, 256, 1024};
     static const double us[] = {0.1, 1.1, 1.3, 1.35, 1.7, 2.5, 6.0};
     if (g <= 1) return us[0];
@@ -673,7 +426,7 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
             for (int g = 1;; g = g * 2 > max_grid && g < max_grid ? max_grid : g * 2) {
                 const int rmax = (a.N + g - 1) / g;
                 if (v == 0 || lds_bytes_for(*in, rmax, true) <= (size_t)max_lds) {
-                    const double t = exchange_us(g) + sweep_us(*in, rmax, v == 1) + 0.3;
+                    const double t = exchange_us_impl(g) + sweep_us(*in, rmax, v == 1) + 0.3;
                     if (t < best) { best = t; grid = g; variant = v; }
                 }
                 if (g >= max_grid) break;
@@ -694,6 +447,22 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     if (e != hipSuccess) return e;
     if (per_cu < 1 || grid > per_cu * num_cus) return hipErrorCooperativeLaunchTooLarge;
     if (grid > kMaxTrainGrid) return hipErrorCooperativeLaunchTooLarge;
+    // The pipelined kernel overlaps the sweep with the exchanges; it is used
+    // only when asked for (variant 3 / 4).
+    if (a.variant == 3 || a.variant == 4) {
+        const double own = exchange_us_impl(grid) + sweep_us(*in, rmax, variant == 1) + 0.3;
+        TrainPlan pp;
+        TrainArgs ap = a;
+        ap.variant = a.variant >= 3 ? a.variant - 2 : 0;
+        const double tp = plan_train_pipe(ap, num_cus, max_lds, &pp, exchange_us_impl);
+        if (tp < 1e300 && (tp < own || a.variant >= 3)) {
+            *plan = pp;
+            plan->kslots = in->k;
+            return hipSuccess;
+        }
+        if (a.variant >= 3) return hipErrorInvalidValue;
+    }
+    plan->pipe_m = 0;
     plan->grid = grid;
     // measured: one slot per 128-byte line is fastest up to 64 workgroups,
     // 32-byte spacing beyond
@@ -706,6 +475,7 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
 }
 
 hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s) {
+    if (plan.variant >= 2) return launch_train_pipe(a, plan, s);
     const Instance *in = pick(a.ld / 4);
     if (!in || in->k != plan.kslots || (int64_t)in->lanes * in->k != a.ld / 4)
         return hipErrorInvalidValue;

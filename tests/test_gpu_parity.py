@@ -189,12 +189,34 @@ def test_infinite_radius_moves_every_unit_alike():
     m.close()
 
 
+def test_near_duplicate_samples_in_one_block_keep_their_bmu():
+    # With sigma = 0 and lr = 1 each step copies its sample into the BMU; the
+    # next sample differs from it by ~1e-4 per element, so that unit is
+    # closer than any other by orders of magnitude even though, in Gram
+    # form, its fp32 distance is rounding noise around zero (possibly
+    # negative).  Both samples of a pair fall in one block of steps.
+    rng = np.random.default_rng(21)
+    base = rng.random((8, 64)).astype(np.float32)
+    X = np.empty((16, 64), np.float32)
+    X[0::2] = base
+    X[1::2] = base + (1e-4 * rng.standard_normal((8, 64))).astype(np.float32)
+    W = workloads.random_weights(16, 64, 22)
+    order = np.arange(16, dtype=np.int32)
+    m = make_map(4, 4, 64, W=W)
+    trace = dev(np.full(16, -1, dtype=np.int32))
+    m.train(dev(X), 1, 1.0, 1.0, 0.0, 0.0, order=dev(order), bmu_trace=trace)
+    got = trace.cpu().numpy()
+    s = oracle.schedule(1.0, 1.0, 0.0, 0.0, oracle.LINEAR, oracle.LINEAR)
+    Wo, tr = oracle.train(W, 4, 4, X, order, s, trace=True)
+    assert np.array_equal(got, tr)
+    assert np.array_equal(tr[1::2], tr[0::2])
+    assert np.abs(m.weights.cpu().numpy() - Wo).max() == 0.0
+    m.close()
+
+
 # ------------------------------------------------------------ trajectories
-@pytest.mark.parametrize("ci,steps,topology", [(0, 2000, som.RECT), (1, 600, som.RECT),
-                                               (0, 400, som.HEX)])
-def test_bmu_trajectory_matches_oracle_until_first_near_tie(ci, steps, topology):
+def _trajectory_vs_oracle(ci, steps, topology):
     cfg = config(ci)
-    say("trajectory", cfg.name, steps, "hex" if topology else "rect")
     X = workloads.make_data(cfg)
     order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)[:steps]
     T = cfg.steps
@@ -222,6 +244,27 @@ def test_bmu_trajectory_matches_oracle_until_first_near_tie(ci, steps, topology)
         say(f"  final max|dW| = {err:.2e}")
         assert err <= 1e-4
     m.close()
+
+
+@pytest.mark.parametrize("ci,steps,topology", [(0, 2000, som.RECT), (1, 600, som.RECT),
+                                               (0, 400, som.HEX)])
+def test_bmu_trajectory_matches_oracle_until_first_near_tie(ci, steps, topology):
+    say("trajectory", config(ci).name, steps, "hex" if topology else "rect")
+    _trajectory_vs_oracle(ci, steps, topology)
+
+
+@pytest.mark.parametrize("ci,variant", [(0, "3"), (0, "4"), (1, "3"), (1, "4")])
+def test_pipelined_variants_follow_the_oracle(ci, variant, monkeypatch):
+    # variant 3 / 4: the kernel that overlaps the pass over the prototypes
+    # with the grid exchanges (prototypes in LDS / streamed)
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", variant)
+    cfg = config(ci)
+    m = som.Map(cfg.rows, cfg.cols, cfg.d)
+    plan = m.plan()
+    m.close()
+    say("pipelined", cfg.name, plan)
+    assert plan["variant"] == (3 if variant == "3" else 2)
+    _trajectory_vs_oracle(ci, 600, som.RECT)
 
 
 def test_resume_and_determinism_are_bitwise():
