@@ -121,7 +121,9 @@ som_status som_set_stream(som_map *map, void *stream);
 
 /* Online training (paper Sec. 5A and 6C): epochs * n steps over the n x d
  * row-major fp32 device matrix X, as one persistent cooperative kernel that
- * keeps the whole per-sample loop on the device.  Stream-ordered.
+ * keeps the whole per-sample loop on the device.  Stream-ordered.  When d is
+ * not a multiple of 4 or X is not 16-byte aligned, X is first copied into a
+ * buffer of n * roundup(d, 4) floats that the map keeps for later calls.
  * Errors: SOM_E_ARG (map, X or sched NULL, n <= 0, epochs <= 0, epochs * n
  * beyond 2^31 - 1, bad decay kind, lr < 0 or not finite, sigma < 0 or NaN,
  * exponential decay with a zero or infinite endpoint, total_steps too small,

@@ -35,6 +35,10 @@ struct som_map {
     // per-block sample products of the pipelined training kernel
     float *block_dots = nullptr;
     int64_t block_dots_cap = 0;
+    // training copy of X with rows padded to a multiple of 4 floats (used
+    // when d % 4 != 0 or X is not 16-byte aligned)
+    float *xpad = nullptr;
+    int64_t xpad_cap = 0;
     // evaluation scratch
     float *wnorm = nullptr;
     int32_t *cand = nullptr, *idx1 = nullptr, *idx2 = nullptr;
@@ -270,6 +274,7 @@ som_status som_destroy(som_map *m) {
     if (m->order_done) (void)hipEventDestroy(m->order_done);
     (void)hipFree(m->sched);
     (void)hipFree(m->block_dots);
+    (void)hipFree(m->xpad);
     (void)hipFree(m->wnorm);
     (void)hipFree(m->cand);
     (void)hipFree(m->idx1);
@@ -315,7 +320,7 @@ static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
     a.n = n;
     a.slots = m->slots;
     a.state = m->state;
-    a.x_vec4 = (m->d % 4 == 0) && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
+    a.xld = m->d;
     // Launch-shape overrides for tuning sweeps: workgroup count and variant
     // (1 = LDS-resident prototypes, 2 = streamed prototypes).
     const char *g = getenv("SOM_TRAIN_GRID");
@@ -439,6 +444,24 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
             m->block_dots_cap = need;
         }
         a.block_dots = m->block_dots;
+    }
+    if (m->d % 4 != 0 || reinterpret_cast<uintptr_t>(X) % 16 != 0) {
+        // The training kernels read sample rows as aligned float4.
+        const int64_t xld = ((int64_t)m->d + 3) & ~(int64_t)3;
+        if (m->xpad_cap < n * xld) {
+            e = hipStreamSynchronize(m->stream);
+            if (e == hipSuccess && m->xpad) e = hipFree(m->xpad);
+            m->xpad = nullptr;
+            m->xpad_cap = 0;
+            if (e == hipSuccess)
+                e = hipMalloc(reinterpret_cast<void **>(&m->xpad), (size_t)(n * xld) * sizeof(float));
+            if (e != hipSuccess) return from_hip(e);
+            m->xpad_cap = n * xld;
+        }
+        e = som::launch_pad_rows(X, n, m->d, m->xpad, xld, m->stream);
+        if (e != hipSuccess) return from_hip(e);
+        a.X = m->xpad;
+        a.xld = xld;
     }
     a.grid = plan.grid;
     a.slot_spread = plan.slot_spread;

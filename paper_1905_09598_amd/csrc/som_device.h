@@ -114,31 +114,29 @@ __device__ inline unsigned long long wave_argmin_key(unsigned bits, int u0) {
     return ((unsigned long long)m << 32) | (unsigned)(u0 + __builtin_ctzll(hit));
 }
 
+typedef const __attribute__((address_space(1))) float gfloat;
+typedef const __attribute__((address_space(1))) f4 gf4;
+
+// Loads that may fall past the end of a row are made at a clamped column
+// and then replaced by zero with a select: a load under a branch joins the
+// zero of the other path in a copy that waits for the load, which
+// serialises a burst of loads into one memory round trip each.
+__device__ inline f4 load_f4_or_zero(gf4 *row, int q, int n4) {
+    const f4 v = row[q < n4 ? q : n4 - 1];
+    const f4 zero = {0.f, 0.f, 0.f, 0.f};
+    return q < n4 ? v : zero;
+}
+// float4 column q of sample row i (zero past the row's xld / 4 columns).
+__device__ inline f4 sample_f4(const TrainArgs &a, int64_t i, int q) {
+    return load_f4_or_zero((gf4 *)(a.X + i * a.xld), q, (int)(a.xld >> 2));
+}
+
 // Sample row i into the lane's slots; columns past d (row padding) are 0.
 template <int K, int L>
 __device__ inline void load_sample(f4 (&x)[K], const TrainArgs &a, int64_t i) {
     const int li = threadIdx.x % L;
-    if (a.x_vec4) {
-        const f4 *xr = reinterpret_cast<const f4 *>(a.X + i * a.d);
-        const int xd4 = a.d >> 2;  // d % 4 == 0 on this path
 #pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const int q = li + L * k;
-            x[k] = (q < xd4) ? xr[q] : f4{0.f, 0.f, 0.f, 0.f};
-        }
-    } else {
-        const float *xr = a.X + i * a.d;
-#pragma unroll
-        for (int k = 0; k < K; ++k) {
-            const int j = 4 * (li + L * k);
-            f4 v;
-            v.x = (j + 0 < a.d) ? xr[j + 0] : 0.f;
-            v.y = (j + 1 < a.d) ? xr[j + 1] : 0.f;
-            v.z = (j + 2 < a.d) ? xr[j + 2] : 0.f;
-            v.w = (j + 3 < a.d) ? xr[j + 3] : 0.f;
-            x[k] = v;
-        }
-    }
+    for (int k = 0; k < K; ++k) x[k] = sample_f4(a, i, li + L * k);
 }
 
 // Per-step inputs (sample index, schedule entry) are fetched 64 steps at a

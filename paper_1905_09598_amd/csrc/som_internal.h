@@ -32,7 +32,8 @@ struct TrainArgs {
     float *W;               // N x ld, row-major, ld % 4 == 0, zero padding
     int64_t ld;             // row pitch in floats
     int32_t N, d, rows, cols, topology;
-    const float *X;         // n x d, row-major
+    const float *X;         // n x xld, row-major, 16-byte aligned, zero past d
+    int64_t xld;            // row pitch of X in floats, a multiple of 4
     int64_t n;
     const int32_t *order;   // nsteps sample indices
     int64_t nsteps, step0, total_steps;
@@ -46,7 +47,6 @@ struct TrainArgs {
     DevState *state;
     int32_t grid;           // requested workgroups (0 = planner's choice)
     int32_t variant;        // requested variant: 0 any, 1 LDS-resident, 2 streamed
-    int32_t x_vec4;         // X rows may be read as float4 (d % 4 == 0, aligned)
     uint64_t timeout_ticks; // bound of one exchange wait, in 100 MHz ticks
 };
 
@@ -101,6 +101,10 @@ hipError_t launch_init_uniform(float *W, int64_t ld, int32_t N, int32_t d,
 hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, hipStream_t s);
 hipError_t launch_row_sqnorm(const float *W, int64_t ld, int32_t N, float *out,
                              hipStream_t s);
+// Copy the n x d rows of X into out, rows of xld floats (xld >= d, a
+// multiple of 4), zero past d.
+hipError_t launch_pad_rows(const float *X, int64_t n, int32_t d, float *out, int64_t xld,
+                           hipStream_t s);
 
 struct EvalArgs {
     const float *W;

@@ -82,14 +82,13 @@ __device__ inline void sweep(f4 *rows_p, int R, const f4 (&xu)[M][K], const f4 (
     const int tid = threadIdx.x, g = tid / L, li = tid % L, lane = tid & 63, wig = li >> 6;
     for (int rb = g; rb < R; rb += P * U) {
         f4 w[U][K];
+        // unconditional loads (clamped row, unused past R): see load_f4_or_zero
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int r = rb + u * P;
-            if (r < R) {
-                const row_t<LDSW> *row = rows + (size_t)r * P4 + li;
+            const int r = rb + u * P < R ? rb + u * P : R - 1;
+            const row_t<LDSW> *row = rows + (size_t)r * P4 + li;
 #pragma unroll
-                for (int k = 0; k < K; ++k) w[u][k] = row[L * k];
-            }
+            for (int k = 0; k < K; ++k) w[u][k] = row[L * k];
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -447,17 +446,17 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     if (e != hipSuccess) return e;
     if (per_cu < 1 || grid > per_cu * num_cus) return hipErrorCooperativeLaunchTooLarge;
     if (grid > kMaxTrainGrid) return hipErrorCooperativeLaunchTooLarge;
-    // The pipelined kernel overlaps the sweep with the exchanges; it is used
-    // only when asked for (variant 3 / 4).
-    if (a.variant == 3 || a.variant == 4) {
-        const double own = exchange_us_impl(grid) + sweep_us(*in, rmax, variant == 1) + 0.3;
+    // The pipelined kernel, which overlaps the pass over the prototypes with
+    // the exchanges, is used wherever its shape limits allow (measured faster
+    // on every such workload); variant 5 keeps this kernel, 3 / 4 require the
+    // pipelined one.
+    if (a.variant == 0 || a.variant == 3 || a.variant == 4) {
         TrainPlan pp;
         TrainArgs ap = a;
         ap.variant = a.variant >= 3 ? a.variant - 2 : 0;
         const double tp = plan_train_pipe(ap, num_cus, max_lds, &pp, exchange_us_impl);
-        if (tp < 1e300 && (tp < own || a.variant >= 3)) {
+        if (tp < 1e300) {
             *plan = pp;
-            plan->kslots = in->k;
             return hipSuccess;
         }
         if (a.variant >= 3) return hipErrorInvalidValue;

@@ -95,6 +95,15 @@ __global__ void row_sqnorm_kernel(const float *W, int64_t ld, int32_t N, float *
     if (lane == 0) out[row] = acc;
 }
 
+__global__ void pad_rows_kernel(const float *X, int64_t n, int32_t d, float *out, int64_t xld) {
+    const int64_t total = n * xld;
+    for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i = e / xld, c = e - i * xld;
+        out[e] = c < d ? X[i * d + c] : 0.f;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_init_uniform(float *W, int64_t ld, int32_t N, int32_t d,
@@ -127,6 +136,15 @@ hipError_t launch_row_sqnorm(const float *W, int64_t ld, int32_t N, float *out,
     const int waves = 4;
     const int64_t blocks = (N + waves - 1) / waves;
     row_sqnorm_kernel<<<dim3((unsigned)blocks), dim3(64 * waves), 0, s>>>(W, ld, N, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_pad_rows(const float *X, int64_t n, int32_t d, float *out, int64_t xld,
+                           hipStream_t s) {
+    const int64_t total = n * xld;
+    int64_t blocks = (total + 255) / 256;
+    if (blocks > 65536) blocks = 65536;
+    pad_rows_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(X, n, d, out, xld);
     return hipGetLastError();
 }
 
