@@ -10,10 +10,12 @@ Data, order and initial prototypes are resident in HBM before timing starts.
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload I]
 
 prints one JSON line.  `value` is prototype*dim updates per second of the
-whole step, T * N * d / step time.  `roofline` reports the training
-kernel: algorithmic bytes 3 * N * d * 4 per sample (read the prototypes for
-the distance, read and write them for the update) divided by the kernel's
-average duration from HIP events on its stream, against the 8 TB/s HBM peak.
+whole step, T * N * d / step time.  `roofline` reports the training call:
+algorithmic bytes 3 * N * d * 4 per sample (read the prototypes for the
+distance, read and write them for the update) divided by the average
+duration of som_train's kernels (schedule table, per-block sample products
+where used, the persistent training kernel) from HIP events on their
+stream, against the 8 TB/s HBM peak.
 `cpu_baseline` times the fp64 oracle on the host over a bounded prefix of
 the same training run.
 """
@@ -29,12 +31,18 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "train_kernel_traffic.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_1905_09598_amd", "csrc", "som_train.hip")
+TRAIN_SOURCES = [os.path.join(ROOT, "paper_1905_09598_amd", "csrc", f)
+                 for f in ("som_device.h", "som_internal.h", "som_train.hip",
+                           "som_train_pipe.hip")]
 
 
 def kernel_source_sha() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """sha256 over the training kernels' sources (in a fixed order)."""
+    h = hashlib.sha256()
+    for path in TRAIN_SOURCES:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic(workload: str):
