@@ -66,6 +66,31 @@ __device__ inline void wave_sums(float (&v)[U]) {
         v[u] = (lane_f(v[u], 0) + lane_f(v[u], 16)) + (lane_f(v[u], 32) + lane_f(v[u], 48));
 }
 
+// As wave_sums, but the sums are complete only in lane 63: after the row
+// butterflies, row_bcast:15 adds each row's last lane into rows 1 and 3 and
+// row_bcast:31 adds lane 31 into rows 2 and 3 (six DPP adds per value
+// instead of four adds, four lane reads and three adds).
+template <int CTRL, int ROWS>
+__device__ inline float dpp_add_rows(float v) {
+    return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xf,
+                                                          false));
+}
+template <int U>
+__device__ inline void wave_sums_last(float (&v)[U]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0xB1>(v[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x4E>(v[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x141>(v[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_pair<0x140>(v[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_add_rows<0x142, 0xa>(v[u]);  // row_bcast:15
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = dpp_add_rows<0x143, 0xc>(v[u]);  // row_bcast:31
+}
+
 __device__ inline unsigned long long u64_min(unsigned long long a, unsigned long long b) {
     return a < b ? a : b;
 }

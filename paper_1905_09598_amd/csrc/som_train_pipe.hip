@@ -34,6 +34,8 @@
 // products over its lanes and the controller adds the three partials.  Rows
 // are loaded a few rows ahead of their use.  The next block's samples are
 // loaded at the end of a sweep, while the sweepers wait for the controller.
+// The samples stay raw (centred per use, as the prepass does), so that a
+// unit rate with a zero radius still copies a sample bit-exactly.
 #include "som_device.h"
 
 namespace som {
@@ -158,8 +160,9 @@ __device__ inline float dot4(f4 a, f4 b, float acc) {
 // materialises w <- beta w + sum_i gamma_i xp_i from coef_prev; then with
 // z = xc_0 and f = w - z it accumulates f.f, f.(xc_i - z) for i >= 1 (ADOT)
 // and f.(xn_j - z) (BDOT), reduced over the wave into
-// dots[(r * 3 + sweeper) * 2M + ...].  Rows (and their coefficients) are
-// loaded D rows ahead, into a ring of registers indexed statically.
+// dots[(r * 3 + sweeper) * 2M + ...] (complete in lane 63).  Rows (and their
+// coefficients) are loaded D rows ahead, into a ring of registers indexed
+// statically.
 template <int M, int KS, int D, bool LDSW, bool MAT, bool ADOT, bool BDOT>
 __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&xp)[M][KS],
                                   const f4 (&xc)[M][KS], const f4 (&xn)[M][KS],
@@ -231,8 +234,8 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
                 }
                 issue(r + D, ring[u], cring[u]);
                 if (DOTS) {
-                    wave_sums<ND>(acc);
-                    if (lane == 0)
+                    wave_sums_last<ND>(acc);
+                    if (lane == 63)
 #pragma unroll
                         for (int t = 0; t < ND; ++t) dots[(r * kSweepers + s) * ND + t] = acc[t];
                 }
@@ -356,6 +359,13 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
                 l.dots + ((size_t)(par ^ 1) * l.Rp + (lane < R ? lane : 0)) * kSweepers * ND;
 #pragma unroll
             for (int t = 0; t < ND; ++t) d[t] = (dr[t] + dr[ND + t]) + dr[2 * ND + t];
+            if (blk == 0) {
+                // the initial prototypes' products with block 0 itself:
+                // f.B_j = f.A_j (B_0 = A_0 = 0)
+                d[M] = 0.f;
+#pragma unroll
+                for (int j = 1; j < M; ++j) d[M + j] = d[j];
+            }
             gram_from_dots<M>(d, beta_prev, gam_prev, AA, AB, BB, E);
             if (blk + 1 < nb) sd.load(a.block_dots, blk, nb);
             const int64_t s0 = blk * M;
@@ -376,15 +386,15 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
             if (bc->abort) return;
         }
     } else {
-        StepWindow<int> ow;
-        ow.init(a, 0);
+        StepWindow<int> own;
+        own.init(a, 0);
         // Slices of the samples of the previous, current and next block.
         f4 xp[M][KS], xc[M][KS], xn[M][KS];
-        load_samples<M, KS>(xc, a, 0, ow);
-        if (nb > 1) load_samples<M, KS>(xn, a, 1, ow);
+        load_samples<M, KS>(xc, a, 0, own);
+        if (nb > 1) load_samples<M, KS>(xn, a, 1, own);
         // Products of the initial prototypes with block 0 (centred on its
-        // first sample), parity 1.
-        pipe_sweep<M, KS, D, LDSW, false, false, true>(rows, R, P4, nw, xc, xc, xc, l.coef,
+        // first sample): f.f and f.(x_{0,i} - z), parity 1.
+        pipe_sweep<M, KS, D, LDSW, false, true, false>(rows, R, P4, nw, xc, xc, xc, l.coef,
                                                        l.dots + (size_t)l.Rp * kSweepers * ND);
         __syncthreads();
         for (int64_t blk = 0; blk < nb; ++blk) {
@@ -407,7 +417,7 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
                     xp[j][t] = xc[j][t];
                     xc[j][t] = xn[j][t];
                 }
-            if (blk + 2 < nb) load_samples<M, KS>(xn, a, blk + 2, ow);
+            if (blk + 2 < nb) load_samples<M, KS>(xn, a, blk + 2, own);
             __syncthreads();
             if (bc->abort) return;
         }
