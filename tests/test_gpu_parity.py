@@ -373,3 +373,57 @@ def test_tiny_and_ragged_maps_train_like_the_oracle():
             Ds = np.sort(oracle.distances(Wk, X[order[k]]))
             assert (Ds[1] - Ds[0]) / Ds[0] <= GAP
         m.close()
+
+
+def _train_vs_oracle(rows, cols, d, n, epochs, topology=som.RECT, seed=3):
+    X = workloads.gaussian_mixture(n, d, 4, 0.15, seed=seed)
+    order = workloads.epoch_orders(n, epochs, seed)
+    s = oracle.schedule(0.4, 0.02, max(rows, cols) / 2.0, 0.5)
+    W0 = oracle.init_uniform(seed, rows * cols, d)
+    m = som.Map(rows, cols, d, seed=seed, topology=topology)
+    plan = m.plan()
+    trace = dev(np.full(epochs * n, -1, np.int32))
+    m.train(dev(X), epochs, 0.4, 0.02, max(rows, cols) / 2.0, 0.5, order=dev(order),
+            bmu_trace=trace)
+    got = trace.cpu().numpy()
+    Wo, tr = oracle.train(W0, rows, cols, X, order, s, topology=topology, trace=True)
+    if np.array_equal(got, tr):
+        err = np.abs(m.weights.cpu().numpy().astype(np.float64) - Wo).max()
+        say(f"  plan {plan}: identical BMUs for {len(tr)} steps, max|dW| = {err:.2e}")
+        assert err <= 1e-4
+    else:
+        k = int(np.argmax(got != tr))
+        say(f"  plan {plan}: identical BMUs for {k}/{len(tr)} steps")
+        Wk, _ = oracle.train(W0, rows, cols, X, order[:k], s, total_steps=epochs * n,
+                             topology=topology)
+        Ds = np.sort(oracle.distances(Wk, X[order[k]]))
+        assert (Ds[1] - Ds[0]) / Ds[0] <= GAP, "divergence without a near tie"
+    m.close()
+    return plan
+
+
+# Shapes chosen to reach the kernels' edges: one float4 slice per row (two
+# sweepers idle), ragged last slices, a partial last block of steps, 64 units
+# per workgroup, and rows too long for the pipelined kernel's registers.
+@pytest.mark.parametrize("rows,cols,d,n,epochs", [
+    (7, 9, 64, 101, 2),       # one slice, M = 8, 202 steps (partial last block)
+    (12, 12, 777, 83, 2),     # 4 slices (2 / 1 / 1 per sweeper), ragged last float4
+    (20, 13, 1500, 61, 2),    # 6 - 8 slices
+    (9, 50, 2048, 40, 1),     # 8 slices, 2 units per workgroup
+    (128, 128, 16, 20, 1),    # 64 units per workgroup
+    (6, 5, 3000, 30, 2),      # rows too long for the pipelined kernel
+])
+@pytest.mark.parametrize("variant", ["0", "3", "4", "5"])
+def test_training_shapes_follow_the_oracle(rows, cols, d, n, epochs, variant, monkeypatch):
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", variant)
+    say("shape", rows, cols, d, n, epochs, "variant", variant)
+    try:
+        plan = _train_vs_oracle(rows, cols, d, n, epochs)
+    except som.SomError as e:
+        if variant in ("3", "4") and e.name == "SOM_E_UNSUPPORTED":
+            pytest.skip("shape outside the pipelined kernel's limits")
+        raise
+    if variant in ("3", "4"):
+        assert plan["variant"] == (3 if variant == "3" else 2)
+    if variant == "5":
+        assert plan["variant"] in (0, 1)
