@@ -109,13 +109,15 @@ __device__ inline unsigned wave_min_u32(unsigned v) {
 }
 
 // Minimum of a 64-bit key over the wave: the high words first, then the low
-// words among the lanes that hold the minimal high word (usually one).
-__device__ inline unsigned long long wave_min_key(unsigned long long v) {
+// words among the lanes that hold the minimal high word.  When the low words
+// increase with the lane (lanes_ordered), or only one lane holds the minimal
+// high word, that is the low word of the first such lane.
+__device__ inline unsigned long long wave_min_key(unsigned long long v, bool lanes_ordered) {
     const unsigned hi = (unsigned)(v >> 32), lo = (unsigned)v;
     const unsigned mh = wave_min_u32(hi);
     const unsigned long long hit = __ballot(hi == mh);
     unsigned ml;
-    if (__builtin_popcountll(hit) == 1)
+    if (lanes_ordered || __builtin_popcountll(hit) == 1)
         ml = (unsigned)__builtin_amdgcn_readlane((int)lo, __builtin_ctzll(hit));
     else
         ml = wave_min_u32(hi == mh ? lo : 0xffffffffu);
@@ -287,7 +289,9 @@ __device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long
             }
         }
     }
-    m = wave_min_key(m);
+    // With at most 64 workgroups lane i holds workgroup i's key, and
+    // workgroups own increasing unit ranges.
+    m = wave_min_key(m, G <= 64);
     if (__ballot(abort) != 0) return -1;
     return (int)(m & (unsigned long long)kMaxUnits);
 }
@@ -307,7 +311,9 @@ __device__ inline float neighbour_h(const TrainArgs &a, float4 p, float cr, floa
     } else {
         g = dr * dr + dx * dx;
     }
-    return lr * exp2f(-g * c2);
+    // v_exp_f32 directly: results below the normal range flush to zero
+    // (a neighbourhood factor under 2^-126 moves nothing in fp32 anyway).
+    return lr * __builtin_amdgcn_exp2f(-g * c2);
 }
 
 // One wave per workgroup runs the mb steps s0 .. s0 + mb - 1 of a block from

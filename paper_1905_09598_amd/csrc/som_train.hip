@@ -211,7 +211,7 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
             const float D = fmaf(-2.f, lin, Er[tri(k, k)]) + quad;
             best = u64_min(best, row_key(D, r0 + r));
         }
-        best = wave_min_key(best);
+        best = wave_min_key(best, false);
         const int c = exchange(a, s, best);
         if (c < 0) return false;
         if (blockIdx.x == 0 && lane == 0 && a.bmu_trace) a.bmu_trace[s] = c;

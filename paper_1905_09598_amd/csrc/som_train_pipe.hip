@@ -383,7 +383,7 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
             for (int j = 0; j < M; ++j) gam_prev[j] = gam[j];
             if (!ok && lane == 0) bc->abort = 1;
             __syncthreads();
-            if (bc->abort) return;
+            if (!ok) return;  // the sweepers read it from bc->abort
         }
     } else {
         StepWindow<int> own;
