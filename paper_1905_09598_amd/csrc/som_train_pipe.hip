@@ -438,21 +438,23 @@ typedef void (*DotsKernel)(TrainArgs, float *, int64_t);
 
 struct PipeInstance {
     int m, ks;
+    bool stream_ok;  // the streamed variant fits in registers
     PipeKernel stream, lds;
     DotsKernel dots;
 };
 
-template <int M, int KS>
+template <int M, int KS, bool STREAM = true>
 constexpr PipeInstance pipe_instance() {
-    return PipeInstance{M, KS, train_pipe_kernel<M, KS, false>, train_pipe_kernel<M, KS, true>,
-                        block_dots_kernel<M>};
+    return PipeInstance{M, KS, STREAM, STREAM ? train_pipe_kernel<M, KS, false> : nullptr,
+                        train_pipe_kernel<M, KS, true>, block_dots_kernel<M>};
 }
 
 // (M, KS): block length and float4 slices of 64 columns per sweeper (rows of
 // up to 3 * 64 * KS float4).  The sample registers, 3 M KS float4 per lane,
-// bound M * KS.
+// bound M * KS; with KS = 7 only the LDS variant stays out of scratch.
 const PipeInstance kPipe[] = {pipe_instance<8, 1>(), pipe_instance<4, 1>(), pipe_instance<4, 2>(),
-                              pipe_instance<4, 3>(), pipe_instance<2, 3>(), pipe_instance<2, 4>()};
+                              pipe_instance<4, 3>(), pipe_instance<2, 3>(), pipe_instance<2, 4>(),
+                              pipe_instance<2, 7, false>()};
 
 const PipeInstance *pipe_for(int m, int ks) {
     for (const PipeInstance &p : kPipe)
@@ -484,6 +486,7 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
         for (int v = 0; v < 2; ++v) {
             const bool ldsw = v == 1;
             if ((a.variant == 1 && !ldsw) || (a.variant == 2 && ldsw)) continue;
+            if (!ldsw && !pi.stream_ok) continue;
             for (int g = 1;; g = (g * 2 > max_grid && g < max_grid) ? max_grid : g * 2) {
                 const int gg = a.grid > 0 ? (a.grid < a.N ? a.grid : a.N) : g;
                 const int rmax = (a.N + gg - 1) / gg;
@@ -553,6 +556,7 @@ hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStrea
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     PipeKernel fn = plan.variant == 3 ? pi->lds : pi->stream;
+    if (!fn) return hipErrorInvalidValue;
     void *params[] = {&args};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),
                                       dim3(256), params, (unsigned)plan.lds_bytes, s);
