@@ -42,6 +42,7 @@ struct som_map {
     // evaluation scratch
     float *wnorm = nullptr;
     int32_t *cand = nullptr, *idx1 = nullptr, *idx2 = nullptr;
+    int64_t cand_cap = 0;
     float *d1 = nullptr;
     double *sums = nullptr;
     int64_t eval_cap = 0;
@@ -137,12 +138,16 @@ som_status grow(T **p, int64_t count) {
     return from_hip(hipMalloc(reinterpret_cast<void **>(p), (size_t)count * sizeof(T)));
 }
 
-som_status ensure_eval_scratch(som_map *m, int64_t n) {
-    if (n <= m->eval_cap) return SOM_OK;
-    hipError_t e = hipStreamSynchronize(m->stream);
-    if (e != hipSuccess) return from_hip(e);
+som_status ensure_eval_scratch(som_map *m, int64_t n, int64_t ncand) {
+    hipError_t e;
     som_status st;
-    if ((st = grow(&m->cand, n * som::kCand)) != SOM_OK) return st;
+    if (ncand > m->cand_cap) {
+        if ((e = hipStreamSynchronize(m->stream)) != hipSuccess) return from_hip(e);
+        if ((st = grow(&m->cand, ncand)) != SOM_OK) return st;
+        m->cand_cap = ncand;
+    }
+    if (n <= m->eval_cap) return SOM_OK;
+    if ((e = hipStreamSynchronize(m->stream)) != hipSuccess) return from_hip(e);
     if ((st = grow(&m->idx1, n)) != SOM_OK) return st;
     if ((st = grow(&m->idx2, n)) != SOM_OK) return st;
     if ((st = grow(&m->d1, n)) != SOM_OK) return st;
@@ -165,8 +170,6 @@ som_status check_deferred(som_map *m) {
 
 som_status run_eval(som_map *m, const float *X, int64_t n, int32_t *idx1,
                     int32_t *idx2, float *d1) {
-    som_status st = ensure_eval_scratch(m, n);
-    if (st != SOM_OK) return st;
     som::EvalArgs a{};
     a.W = m->W;
     a.ld = m->ld;
@@ -177,6 +180,9 @@ som_status run_eval(som_map *m, const float *X, int64_t n, int32_t *idx1,
     a.topology = m->topology;
     a.X = X;
     a.n = n;
+    som::plan_bmu_candidates(&a);
+    som_status st = ensure_eval_scratch(m, n, n * a.ugroups * som::kCand);
+    if (st != SOM_OK) return st;
     a.wnorm = m->wnorm;
     a.cand = m->cand;
     a.idx1 = idx1;
@@ -476,7 +482,7 @@ som_status som_bmu2(som_map *m, const float *X, int64_t n, int32_t *out_idx,
     if (out_idx && !device_range_ok(out_idx, (uint64_t)n * 4)) return SOM_E_ARG;
     if (out_idx2 && !device_range_ok(out_idx2, (uint64_t)n * 4)) return SOM_E_ARG;
     if (out_d1 && !device_range_ok(out_d1, (uint64_t)n * 4)) return SOM_E_ARG;
-    som_status st = ensure_eval_scratch(m, n);
+    som_status st = ensure_eval_scratch(m, n, 0);
     if (st != SOM_OK) return st;
     return run_eval(m, X, n, out_idx ? out_idx : m->idx1, out_idx2, out_d1);
 }
@@ -488,7 +494,7 @@ som_status som_bmu(som_map *m, const float *X, int64_t n, int32_t *out_idx) {
 
 static som_status qe_te(som_map *m, const float *X, int64_t n, double *qe, double *te) {
     if (!eval_args_ok(m, X, n)) return SOM_E_ARG;
-    som_status st = ensure_eval_scratch(m, n);
+    som_status st = ensure_eval_scratch(m, n, 0);
     if (st != SOM_OK) return st;
     st = run_eval(m, X, n, m->idx1, m->idx2, m->d1);
     if (st != SOM_OK) return st;

@@ -7,9 +7,12 @@
 // only needs s(x, w) = |w|^2 - 2 x.w, and X W^T is an (n x d) by (d x N)
 // matrix product, computed here on the fp32 matrix cores
 // (v_mfma_f32_16x16x4_f32) without ever materialising the n x N matrix: each
-// workgroup keeps, per sample, the kCand units of smallest s.  A second
-// kernel re-ranks those candidates by direct fp32 distances sum (x_j - w_j)^2,
-// which fixes the BMU, the second BMU and the BMU's squared distance.
+// workgroup keeps, per sample, the kCand units of smallest s among its group
+// of units (when there are few samples, the units are split into groups
+// searched by separate workgroups, so that the grid still fills the chip).
+// A second kernel re-ranks the groups' candidates by direct fp32 distances
+// sum (x_j - w_j)^2, which fixes the BMU, the second BMU and the BMU's
+// squared distance.
 #include "som_internal.h"
 
 #include <math.h>
@@ -62,6 +65,9 @@ __global__ __launch_bounds__(kEvalBlock) void bmu_candidates_kernel(EvalArgs a) 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wsamp = wave & 1, wunit = wave >> 1;
     const int64_t s0 = (int64_t)blockIdx.x * kBM;
+    const int grp = blockIdx.y;
+    const int u_begin = grp * a.group_units;
+    const int u_end = u_begin + a.group_units < a.N ? u_begin + a.group_units : a.N;
     const int lrow = lane & 15, lk = (lane >> 4) * 4;
 
     float ts[2][kCand];
@@ -71,7 +77,7 @@ __global__ __launch_bounds__(kEvalBlock) void bmu_candidates_kernel(EvalArgs a) 
 #pragma unroll
         for (int c = 0; c < kCand; ++c) { ts[j][c] = INFINITY; tu[j][c] = -1; }
 
-    for (int u0 = 0; u0 < a.N; u0 += kBN) {
+    for (int u0 = u_begin; u0 < u_end; u0 += kBN) {
         f4 acc[4][2];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -79,7 +85,7 @@ __global__ __launch_bounds__(kEvalBlock) void bmu_candidates_kernel(EvalArgs a) 
             for (int j = 0; j < 2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
 
         __syncthreads();
-        if (tid < kBN) wn[tid] = (u0 + tid < a.N) ? a.wnorm[u0 + tid] : 0.f;
+        if (tid < kBN) wn[tid] = (u0 + tid < u_end) ? a.wnorm[u0 + tid] : 0.f;
 
         for (int k0 = 0; k0 < a.ld; k0 += kBK) {
             __syncthreads();
@@ -112,7 +118,7 @@ __global__ __launch_bounds__(kEvalBlock) void bmu_candidates_kernel(EvalArgs a) 
                 const int64_t unit = u0 + r;
                 const int64_t col = k0 + 4 * c4;
                 f4 v = {0.f, 0.f, 0.f, 0.f};
-                if (unit < a.N && col < a.ld)
+                if (unit < u_end && col < a.ld)
                     v = *reinterpret_cast<const f4 *>(a.W + unit * a.ld + col);
                 *reinterpret_cast<f4 *>(&ws[r * kLdsStride + 4 * c4]) = v;
             }
@@ -150,7 +156,7 @@ __global__ __launch_bounds__(kEvalBlock) void bmu_candidates_kernel(EvalArgs a) 
             for (int v = 0; v < 4; ++v) {
                 const int ul = wunit * 64 + i * 16 + (lane >> 4) * 4 + v;
                 const int u = u0 + ul;
-                if (u < a.N) {
+                if (u < u_end) {
 #pragma unroll
                     for (int j = 0; j < 2; ++j)
                         insert_top(ts[j], tu[j], wn[ul] - 2.f * acc[i][j][v], u);
@@ -180,7 +186,8 @@ __global__ __launch_bounds__(kEvalBlock) void bmu_candidates_kernel(EvalArgs a) 
             if (cd.u >= 0) insert_top(ms, mu, cd.s, cd.u);
         }
 #pragma unroll
-        for (int c = 0; c < kCand; ++c) a.cand[(s0 + tid) * kCand + c] = mu[c];
+        for (int c = 0; c < kCand; ++c)
+            a.cand[((s0 + tid) * a.ugroups + grp) * kCand + c] = mu[c];
     }
 }
 
@@ -194,9 +201,9 @@ __global__ __launch_bounds__(64 * kRerankWaves) void bmu_rerank_kernel(EvalArgs 
     const float *x = a.X + i * a.d;
     float bd = INFINITY, sd = INFINITY;
     int bu = -1, su = -1;
-#pragma unroll
-    for (int c = 0; c < kCand; ++c) {
-        const int u = a.cand[i * kCand + c];
+    const int nc = a.ugroups * kCand;
+    for (int c = 0; c < nc; ++c) {
+        const int u = a.cand[i * nc + c];
         if (u < 0) continue;  // same for the whole wave
         const float *w = a.W + (int64_t)u * a.ld;
         float acc = 0.f;
@@ -251,9 +258,25 @@ __global__ __launch_bounds__(kReduceBlock) void qe_te_reduce_kernel(
 
 }  // namespace
 
+void plan_bmu_candidates(EvalArgs *a) {
+    const int64_t tiles = (a->n + kBM - 1) / kBM;
+    const int64_t unit_tiles = (a->N + kBN - 1) / kBN;
+    // aim at two workgroups per compute unit
+    int64_t g = (512 + tiles - 1) / tiles;
+    if (g > unit_tiles) g = unit_tiles;
+    if (g < 1) g = 1;
+    const int64_t tiles_per_group = (unit_tiles + g - 1) / g;
+    a->group_units = (int32_t)(tiles_per_group * kBN);
+    a->ugroups = (int32_t)((a->N + a->group_units - 1) / a->group_units);
+}
+
 hipError_t launch_bmu_candidates(const EvalArgs &a, hipStream_t s) {
     const int64_t blocks = (a.n + kBM - 1) / kBM;
-    bmu_candidates_kernel<<<dim3((unsigned)blocks), dim3(kEvalBlock), 0, s>>>(a);
+    if (a.ugroups < 1 || a.group_units % kBN != 0 ||
+        (int64_t)a.ugroups * a.group_units < a.N)
+        return hipErrorInvalidValue;
+    bmu_candidates_kernel<<<dim3((unsigned)blocks, (unsigned)a.ugroups), dim3(kEvalBlock), 0, s>>>(
+        a);
     return hipGetLastError();
 }
 

@@ -113,7 +113,9 @@ struct EvalArgs {
     const float *X;
     int64_t n;
     const float *wnorm;     // N squared prototype norms
-    int32_t *cand;          // n x kCand candidate units (scratch)
+    int32_t *cand;          // n x ugroups x kCand candidate units (scratch)
+    int32_t ugroups;        // unit groups searched by separate workgroups
+    int32_t group_units;    // units per group (a multiple of the unit tile)
     int32_t *idx1;          // n (required)
     int32_t *idx2;          // n (nullable)
     float *d1;              // n (nullable)
@@ -121,6 +123,9 @@ struct EvalArgs {
 };
 constexpr int kCand = 4;
 
+// Unit groups for n samples over N units: enough workgroups to fill the
+// chip when n is small (sets a->ugroups and a->group_units).
+void plan_bmu_candidates(EvalArgs *a);
 hipError_t launch_bmu_candidates(const EvalArgs &a, hipStream_t s);
 hipError_t launch_bmu_rerank(const EvalArgs &a, hipStream_t s);
 // QE and TE sums over n samples from (idx1, idx2, d1); writes 2 doubles.
