@@ -427,3 +427,34 @@ def test_training_shapes_follow_the_oracle(rows, cols, d, n, epochs, variant, mo
         assert plan["variant"] == (3 if variant == "3" else 2)
     if variant == "5":
         assert plan["variant"] in (0, 1)
+
+
+def test_misaligned_samples_train_like_aligned_ones():
+    # X starting one float into an allocation (d % 4 == 0 but rows not
+    # 16-byte aligned) goes through the padded copy; results are bitwise
+    # those of the aligned matrix.
+    torch = torch_cuda()
+    n, d = 90, 256
+    X = workloads.gaussian_mixture(n, d, 3, 0.2, seed=11)
+    order = dev(workloads.epoch_orders(n, 2, 5))
+    flat = torch.zeros(n * d + 1, dtype=torch.float32, device="cuda")
+    flat[1:] = torch.from_numpy(X.reshape(-1)).cuda()
+    Xm = flat[1:].view(n, d)
+    assert Xm.data_ptr() % 16 != 0
+    out = []
+    for Xd in (dev(X), Xm):
+        m = som.Map(6, 7, d, seed=4)
+        trace = dev(np.full(2 * n, -1, np.int32))
+        m.train(Xd, 2, 0.5, 0.05, 3.0, 0.5, order=order, bmu_trace=trace)
+        out.append((m.weights.cpu().numpy(), trace.cpu().numpy()))
+        m.close()
+    assert np.array_equal(out[0][1], out[1][1])
+    assert np.array_equal(out[0][0], out[1][0])
+
+
+@pytest.mark.parametrize("variant", ["0", "5"])
+def test_hexagonal_lattice_shapes_follow_the_oracle(variant, monkeypatch):
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", variant)
+    for rows, cols, d, n in ((9, 11, 300, 70), (16, 16, 1024, 40)):
+        say("hex shape", rows, cols, d, n, "variant", variant)
+        _train_vs_oracle(rows, cols, d, n, 2, topology=som.HEX)
