@@ -30,6 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "train_kernel_traffic.json")
 TRAIN_SOURCES = [os.path.join(ROOT, "paper_1905_09598_amd", "csrc", f)
                  for f in ("som_device.h", "som_internal.h", "som_train.hip",
@@ -86,6 +87,59 @@ def cpu_baseline(cfg, X, order, budget_s: float):
     }
 
 
+def map_sweep(cpu_budget: float):
+    """Per-step training time against map size at d = 64: an analogue of the
+    paper's Table 3 (time against map size), on synthetic data: n = 8192
+    samples of a 16-cluster Gaussian mixture (sd 0.2), one epoch, lr 0.5 ->
+    0.01 linear, sigma side/2 -> 1 exponential, seeded as the workloads are."""
+    import torch
+
+    import oracle
+    import paper_1905_09598_amd as som
+    import workloads
+
+    n, d = 8192, 64
+    X = workloads.gaussian_mixture(n, d, 16, 0.2, seed=7)
+    order = workloads.epoch_orders(n, 1, 7)
+    Xd = torch.from_numpy(X).cuda()
+    od = torch.from_numpy(order).cuda()
+    stream = torch.cuda.current_stream()
+    for side in (16, 32, 64, 128, 256, 512):
+        N = side * side
+        m = som.Map(side, side, d, seed=0)
+        plan = m.plan()
+        kw = dict(order=od)
+        m.train(Xd, 1, 0.5, 0.01, side / 2.0, 1.0, **kw)  # warm-up
+        times = []
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            m.train(Xd, 1, 0.5, 0.01, side / 2.0, 1.0, **kw)
+            b.record(stream)
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b) / 1e3)
+        t = sorted(times)[1]
+        line = {"map": f"{side}x{side}", "units": N, "d": d, "steps": n,
+                "us_per_step": t / n * 1e6, "proto_dim_updates_per_s": n * N * d / t,
+                "train_s": t, "grid": plan["grid"],
+                "variant": ["stream", "lds", "pipelined-stream", "pipelined-lds"][plan["variant"]]}
+        if cpu_budget > 0:
+            W = oracle.init_uniform(0, N, d)
+            s_ = oracle.schedule(0.5, 0.01, side / 2.0, 1.0)
+            threads = oracle.default_threads()
+            done, t0 = 0, time.perf_counter()
+            while done < n and time.perf_counter() - t0 < cpu_budget / 6:
+                k = min(100, n - done)
+                W, _ = oracle.train(W, side, side, X, order[done:done + k], s_, step0=done,
+                                    total_steps=n, nthreads=threads)
+                done += k
+            dt = time.perf_counter() - t0
+            line["oracle_us_per_step"] = dt / done * 1e6
+            line["oracle_cores"] = threads
+        print(json.dumps(line), flush=True)
+        m.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -95,6 +149,9 @@ def main():
                     help="index into the workload table (default: 2000 x 2000 TF-IDF)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
+    ap.add_argument("--map-sweep", action="store_true",
+                    help="instead of the bench line: per-step time of training maps of "
+                         "16x16 ... 512x512 units at d = 64 (one JSON line per map size)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (the "
                          "reference dispatch for scaling HBM byte counters) and exit")
@@ -107,6 +164,9 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes_read": n * 4, "calibrate_copy_bytes_written": n * 4}))
+        return
+    if args.map_sweep:
+        map_sweep(args.cpu_budget)
         return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not "
@@ -156,6 +216,18 @@ def main():
     wall = time.perf_counter() - t0
 
     train_ms = [a.elapsed_time(b) for a, b in events]
+
+    # Batched BMU (the evaluation's dense contraction X W^T on fp32 MFMA):
+    # som_bmu over all n samples, timed with HIP events on the same stream.
+    bmu_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(3)]
+    for a, b in bmu_ev:
+        a.record(stream)
+        m.bmu(Xd)
+        b.record(stream)
+    torch.cuda.synchronize()
+    bmu_s = min(a.elapsed_time(b) for a, b in bmu_ev) / 1e3
+    bmu_flops = 2.0 * cfg.n * cfg.units * cfg.d
     avg_train_s = sum(train_ms) / len(train_ms) / 1e3
     updates = cfg.steps * cfg.units * cfg.d
     ms_per_step = wall / args.steps * 1e3
@@ -195,6 +267,13 @@ def main():
                        "train_pipe_kernel (stream)", "train_pipe_kernel (lds)"][plan["variant"]],
             "kernel_ms": avg_train_s * 1e3,
             "alg_bytes_per_launch": alg_bytes,
+        },
+        "bmu_mfma": {
+            "achieved": bmu_flops / bmu_s / 1e12, "peak": FP32_MFMA_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": bmu_flops / bmu_s / 1e12 / FP32_MFMA_PEAK_TFLOPS,
+            "flops": bmu_flops, "ms": bmu_s * 1e3,
+            "note": "som_bmu over all n samples: 2 n N d flops of X W^T (fp32 MFMA) plus "
+                    "the candidate re-rank, best of 3",
         },
         "train_ms": avg_train_s * 1e3,
         "us_per_sample_step": avg_train_s / cfg.steps * 1e6,

@@ -128,7 +128,10 @@ som_status som_set_stream(som_map *map, void *stream);
  * beyond 2^31 - 1, bad decay kind, lr < 0 or not finite, sigma < 0 or NaN,
  * exponential decay with a zero or infinite endpoint, total_steps too small,
  * X, order or bmu_trace not covering their extent), SOM_E_UNSUPPORTED
- * (d above the largest built kernel shape), SOM_E_LAUNCH, SOM_E_DEVICE.
+ * (d above the largest built kernel shape, or more units per workgroup than
+ * the kernels' per-unit LDS state holds: 4096 per workgroup for d <= 256
+ * and at least 690 otherwise, i.e. 1,048,576 and 176,640 units on 256
+ * workgroups), SOM_E_LAUNCH, SOM_E_DEVICE.
  * An order entry outside [0, n) stops the kernel before any update and is
  * reported as SOM_E_BAD_ORDER by the next synchronizing call. */
 som_status som_train(som_map *map, const float *X, int64_t n, int32_t epochs,

@@ -438,7 +438,7 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
     }
     a.sched = m->sched;
     if (plan.variant >= 2) {
-        const int64_t need = som::pipe_block_dots_floats(plan.pipe_m, nsteps);
+        const int64_t need = som::pipe_block_dots_floats(plan.block_m, nsteps);
         if (m->block_dots_cap < need) {
             e = hipStreamSynchronize(m->stream);
             if (e == hipSuccess && m->block_dots) e = hipFree(m->block_dots);

@@ -54,7 +54,7 @@ struct TrainPlan {
     int32_t grid = 0;
     int32_t block = kTrainBlock;
     int32_t variant = 0;     // 0 streamed, 1 LDS-resident, 2 / 3 pipelined streamed / LDS
-    int32_t pipe_m = 0;      // block length of the pipelined variants
+    int32_t block_m = 0;     // steps per block of the chosen kernel instance
     int32_t kslots = 0;      // float4 columns per lane (template instance)
     int32_t slot_spread = 1;
     size_t lds_bytes = 0;

@@ -347,8 +347,12 @@ constexpr Instance instance() {
 
 // Row pitch L * K float4 (d up to 4 L K floats) and block length M, sized so
 // the two blocks of samples (2 M K float4 per lane) stay in registers.
+// Per row length (lanes x k) the first instance is preferred; later ones of
+// the same row length (shorter blocks, less LDS per owned row) serve maps
+// whose workgroups own too many rows for the first.
 const Instance kInstances[] = {
-    instance<64, 1, 8, 1>(),   instance<64, 2, 8, 1>(),   instance<64, 4, 4, 1>(),
+    instance<64, 1, 8, 1>(),   instance<64, 1, 4, 1>(),   instance<64, 1, 2, 1>(),
+    instance<64, 2, 8, 1>(),   instance<64, 4, 4, 1>(),
     instance<128, 4, 4, 2>(),  instance<256, 3, 4, 1>(),  instance<256, 4, 4, 1>(),
     instance<256, 5, 3, 1>(),  instance<256, 6, 2, 1>(),  instance<256, 8, 2, 1>(),
     instance<256, 10, 2, 1>(), instance<256, 12, 1, 1>(), instance<256, 16, 1, 1>(),
@@ -405,12 +409,23 @@ int64_t train_row_pitch(int32_t d) {
 
 hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     const int64_t ld4 = a.ld / 4;
-    const Instance *in = pick(ld4);
-    if (!in || (int64_t)in->lanes * in->k != ld4) return hipErrorInvalidValue;
     int max_lds = 0;
     hipError_t e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, 0);
     if (e != hipSuccess) return e;
     const int max_grid = a.N < num_cus ? a.N : num_cus;
+    // first instance of this row length whose per-row state fits in LDS at
+    // the largest grid (or the requested one)
+    const Instance *in = nullptr;
+    {
+        const int g = a.grid > 0 ? (a.grid < a.N ? a.grid : a.N) : max_grid;
+        const int rmax = (a.N + g - 1) / g;
+        for (const Instance &c : kInstances)
+            if ((int64_t)c.lanes * c.k == ld4 && lds_bytes_for(c, rmax, false) <= (size_t)max_lds) {
+                in = &c;
+                break;
+            }
+    }
+    if (!in) return hipErrorInvalidValue;
 
     int grid = 0, variant = 0;
     if (a.grid > 0) {
@@ -461,7 +476,6 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
         }
         if (a.variant >= 3) return hipErrorInvalidValue;
     }
-    plan->pipe_m = 0;
     plan->grid = grid;
     // measured: one slot per 128-byte line is fastest up to 64 workgroups,
     // 32-byte spacing beyond
@@ -469,15 +483,20 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     plan->block = kTrainBlock;
     plan->variant = variant;
     plan->kslots = in->k;
+    plan->block_m = in->m;
     plan->lds_bytes = lds;
     return hipSuccess;
 }
 
 hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s) {
     if (plan.variant >= 2) return launch_train_pipe(a, plan, s);
-    const Instance *in = pick(a.ld / 4);
-    if (!in || in->k != plan.kslots || (int64_t)in->lanes * in->k != a.ld / 4)
-        return hipErrorInvalidValue;
+    const Instance *in = nullptr;
+    for (const Instance &c : kInstances)
+        if ((int64_t)c.lanes * c.k == a.ld / 4 && c.m == plan.block_m) {
+            in = &c;
+            break;
+        }
+    if (!in || in->k != plan.kslots) return hipErrorInvalidValue;
     TrainArgs args = a;
     args.grid = plan.grid;
     args.slot_spread = plan.slot_spread;

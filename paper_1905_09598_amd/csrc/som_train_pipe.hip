@@ -511,7 +511,7 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                         best = t;
                         plan->grid = gg;
                         plan->variant = ldsw ? 3 : 2;
-                        plan->pipe_m = pi.m;
+                        plan->block_m = pi.m;
                         plan->kslots = pi.ks;
                     }
                 }
@@ -520,12 +520,12 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
         }
     }
     if (best < 1e300) {
-        plan->lds_bytes = pipe_lds_bytes(plan->pipe_m, (a.N + plan->grid - 1) / plan->grid, P4,
+        plan->lds_bytes = pipe_lds_bytes(plan->block_m, (a.N + plan->grid - 1) / plan->grid, P4,
                                           plan->variant == 3);
         if (plan->lds_bytes < 84 * 1024) plan->lds_bytes = 84 * 1024;
         plan->block = 256;
         plan->slot_spread = plan->grid <= 64 ? 16 : 4;
-        const PipeInstance *pi = pipe_for(plan->pipe_m, plan->kslots);
+        const PipeInstance *pi = pipe_for(plan->block_m, plan->kslots);
         PipeKernel fn = plan->variant == 3 ? pi->lds : pi->stream;
         int per_cu = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
@@ -542,7 +542,7 @@ int64_t pipe_block_dots_floats(int m, int64_t nsteps) {
 }
 
 hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStream_t s) {
-    const PipeInstance *pi = pipe_for(plan.pipe_m, plan.kslots);
+    const PipeInstance *pi = pipe_for(plan.block_m, plan.kslots);
     if (!pi || !a.block_dots) return hipErrorInvalidValue;
     const int64_t P4 = a.ld / 4;
     if (P4 % 64 != 0 || (P4 / 64 + kSweepers - 1) / kSweepers != pi->ks ||

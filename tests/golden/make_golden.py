@@ -6,9 +6,10 @@ records the final quantization and topographic errors, together with
 checksums of every input so that a test can prove it trains on the same
 bits.
 
-    python tests/golden/make_golden.py CONFIG_INDEX [--threads T]
+    python tests/golden/make_golden.py CONFIG_INDEX [--threads T] [--topology hex]
 
-writes tests/golden/e2e_<config name>.json.
+writes tests/golden/e2e_<config name>.json (e2e_<config name>_hex.json for
+the hexagonal lattice).
 """
 import argparse
 import json
@@ -30,10 +31,12 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("config", type=int)
     ap.add_argument("--threads", type=int, default=oracle.default_threads())
+    ap.add_argument("--topology", choices=("rect", "hex"), default="rect")
     ap.add_argument("--epoch-qe", action="store_true",
                     help="also record the quantization error after every epoch")
     args = ap.parse_args()
     cfg = workloads.WORKLOADS[args.config]
+    topo = oracle.HEX if args.topology == "hex" else oracle.RECT
     t0 = time.time()
     X = workloads.make_data(cfg)
     order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)
@@ -48,17 +51,17 @@ def main():
     for e in range(cfg.epochs):
         sl = order[e * cfg.n:(e + 1) * cfg.n]
         W, _ = oracle.train(W, cfg.rows, cfg.cols, X, sl, s, step0=e * cfg.n,
-                            total_steps=T, nthreads=args.threads)
+                            total_steps=T, topology=topo, nthreads=args.threads)
         msg = f"[golden] {cfg.name}: epoch {e + 1}/{cfg.epochs} " \
               f"at {time.time() - t1:.0f}s"
         if args.epoch_qe:
-            q = oracle.evaluate(W, cfg.rows, cfg.cols, X,
+            q = oracle.evaluate(W, cfg.rows, cfg.cols, X, topology=topo,
                                 nthreads=args.threads)["qe"]
             epoch_qe.append(q)
             msg += f" qe={q:.6f}"
         print(msg, flush=True)
     train_s = time.time() - t1
-    ev = oracle.evaluate(W, cfg.rows, cfg.cols, X, nthreads=args.threads)
+    ev = oracle.evaluate(W, cfg.rows, cfg.cols, X, topology=topo, nthreads=args.threads)
     c1 = ev["c1"]
     rel_gap = np.where(ev["d1"] > 0, (ev["d2"] - ev["d1"]) / np.maximum(ev["d1"], 1e-300),
                        np.inf)
@@ -66,7 +69,7 @@ def main():
         "written_by": "tests/golden/make_golden.py (fp64 oracle only)",
         "config": cfg.name,
         "n": cfg.n, "d": cfg.d, "rows": cfg.rows, "cols": cfg.cols,
-        "epochs": cfg.epochs, "steps": T,
+        "epochs": cfg.epochs, "steps": T, "topology": args.topology,
         "schedule": {"lr0": cfg.lr0, "lr1": cfg.lr1, "lr_decay": "linear",
                      "sigma0": cfg.sigma0, "sigma1": cfg.sigma1,
                      "sigma_decay": "exponential"},
@@ -84,7 +87,8 @@ def main():
         "oracle_threads": args.threads,
         "host": platform.processor() or platform.machine(),
     }
-    path = os.path.join(ROOT, "tests", "golden", f"e2e_{cfg.name}.json")
+    suffix = "_hex" if args.topology == "hex" else ""
+    path = os.path.join(ROOT, "tests", "golden", f"e2e_{cfg.name}{suffix}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
         f.write("\n")

@@ -38,8 +38,8 @@ def oracle_schedule(cfg):
                            oracle.LINEAR, oracle.EXPONENTIAL)
 
 
-def golden(cfg):
-    p = os.path.join(GOLD, f"e2e_{cfg.name}.json")
+def golden(cfg, hex_lattice=False):
+    p = os.path.join(GOLD, f"e2e_{cfg.name}{'_hex' if hex_lattice else ''}.json")
     if not os.path.exists(p):
         return None
     with open(p) as f:

@@ -25,18 +25,20 @@ pytestmark = pytest.mark.gpu
 REL = 0.01
 
 
-@pytest.mark.parametrize("ci", [0, 1, 2, 3, 4])
-def test_full_training_matches_oracle_quality(ci):
+@pytest.mark.parametrize("ci,topology", [(0, som.RECT), (1, som.RECT), (2, som.RECT),
+                                         (3, som.RECT), (4, som.RECT),
+                                         (0, som.HEX), (1, som.HEX), (2, som.HEX)])
+def test_full_training_matches_oracle_quality(ci, topology):
     cfg = config(ci)
-    g = golden(cfg)
+    g = golden(cfg, hex_lattice=topology == som.HEX)
     if g is None:
         pytest.skip(f"no oracle golden values for {cfg.name} yet")
-    say("e2e", cfg.name)
+    say("e2e", cfg.name, "hex" if topology else "rect")
     X = workloads.make_data(cfg)
     order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)
     assert workloads.sha256_of(X) == g["sha256_X"], "input data differs from the golden run"
     assert workloads.sha256_of(order) == g["sha256_order"]
-    m = som.Map(cfg.rows, cfg.cols, cfg.d, seed=cfg.init_seed)
+    m = som.Map(cfg.rows, cfg.cols, cfg.d, seed=cfg.init_seed, topology=topology)
     assert workloads.sha256_of(m.weights.cpu().numpy()) == g["sha256_W0_f32"]
     Xd = dev(X)
     m.train(Xd, cfg.epochs, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1, order=dev(order))
@@ -46,7 +48,7 @@ def test_full_training_matches_oracle_quality(ci):
     # cross-evaluation: the oracle's evaluator on the GPU's trained map
     W = m.weights.cpu().numpy().astype(np.float64)
     sub = slice(0, min(cfg.n, 4000))
-    ev = oracle.evaluate(W, cfg.rows, cfg.cols, X[sub])
+    ev = oracle.evaluate(W, cfg.rows, cfg.cols, X[sub], topology=topology)
     idx = m.bmu(dev(X[sub])).cpu().numpy()
     agree = float(np.mean(idx == ev["c1"]))
     say(f"  cross-eval on {X[sub].shape[0]} samples: BMU agreement {agree:.5f}")

@@ -109,11 +109,12 @@ def test_exact_ties_resolve_to_lowest_index_on_gpu():
 
 
 # ------------------------------------------------------------ one step
+@pytest.mark.parametrize("topology", [som.RECT, som.HEX])
 @pytest.mark.parametrize("ci", [0, 1, 2, 3, 4])
-def test_single_step_update_matches_oracle(ci):
+def test_single_step_update_matches_oracle(ci, topology):
     """Criterion (2): one step from identical state, mid-schedule."""
     cfg = config(ci)
-    say("single-step", cfg.name)
+    say("single-step", cfg.name, "hex" if topology else "rect")
     X = workloads.make_data(cfg)
     rng = np.random.default_rng(ci)
     N = cfg.units
@@ -124,7 +125,7 @@ def test_single_step_update_matches_oracle(ci):
     i = int(rng.integers(0, cfg.n))
     T = cfg.steps
     for t in (0, T // 3, T - 1):
-        m = make_map(cfg.rows, cfg.cols, cfg.d, W=W)
+        m = make_map(cfg.rows, cfg.cols, cfg.d, W=W, topology=topology)
         # a one-step call of a T-step schedule: epochs * n must be 1 -> n = 1
         x1 = X[i:i + 1]
         trace = dev(np.full(1, -7, dtype=np.int32))
@@ -135,8 +136,8 @@ def test_single_step_update_matches_oracle(ci):
         c_gpu = int(trace.cpu().numpy()[0])
         Wo, tr = oracle.train(W.astype(np.float64), cfg.rows, cfg.cols, x1,
                               np.zeros(1, dtype=np.int32), oracle_schedule(cfg),
-                              step0=t, total_steps=T, trace=True)
-        ev = oracle.evaluate(W.astype(np.float64), cfg.rows, cfg.cols, x1)
+                              step0=t, total_steps=T, topology=topology, trace=True)
+        ev = oracle.evaluate(W.astype(np.float64), cfg.rows, cfg.cols, x1, topology=topology)
         if rel_gap(ev["d1"], ev["d2"])[0] > GAP:
             assert c_gpu == tr[0]
         if c_gpu == tr[0]:
@@ -458,3 +459,11 @@ def test_hexagonal_lattice_shapes_follow_the_oracle(variant, monkeypatch):
     for rows, cols, d, n in ((9, 11, 300, 70), (16, 16, 1024, 40)):
         say("hex shape", rows, cols, d, n, "variant", variant)
         _train_vs_oracle(rows, cols, d, n, 2, topology=som.HEX)
+
+
+@pytest.mark.parametrize("side", [128, 512])
+def test_large_maps_at_small_d_follow_the_oracle(side):
+    # Maps of the d = 64 size sweep: 16384 units (64 per workgroup) and
+    # 262144 units (1024 per workgroup, the blocked kernel's LDS loop path).
+    say("large map", side, side)
+    _train_vs_oracle(side, side, 64, 150, 1)
