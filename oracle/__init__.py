@@ -188,3 +188,65 @@ def evaluate(W: np.ndarray, rows: int, cols: int, X: np.ndarray,
         raise ValueError(f"som_oracle_evaluate: bad arguments (rc={rc})")
     return {"c1": c1, "c2": c2, "d1": d1, "d2": d2, "qe": qe.value,
             "te": te.value}
+
+
+# ------------------------------------------------------------------ linear init
+# Sec. 6D: the prototypes start as a regular two-dimensional grid in the
+# hyperplane spanned by the two largest principal components of the data;
+# Fig. 2 derives the map size and the iteration count from the data size and
+# those components.  Plain numpy in fp64; the eigen-decomposition is numpy's.
+
+def pca_top2(X: np.ndarray):
+    """Fig. 2 steps 3-4: the two largest eigenvalues lambda1 >= lambda2 of the
+    covariance (1/m) sum_i (x_i - mu)(x_i - mu)^T of the m rows of X, their
+    unit eigenvectors (columns of V; sign fixed so that the component of
+    largest magnitude, lowest index on ties, is positive) and the mean mu."""
+    X64 = np.asarray(X, dtype=np.float64)
+    m = X64.shape[0]
+    mu = X64.mean(axis=0)
+    Xc = X64 - mu
+    Cov = Xc.T @ Xc / m
+    w, V = np.linalg.eigh(Cov)  # ascending
+    lam = w[::-1][:2].copy()
+    V = V[:, ::-1][:, :2].copy()
+    for a in range(V.shape[1]):
+        k = int(np.argmax(np.abs(V[:, a])))
+        if V[k, a] < 0:
+            V[:, a] = -V[:, a]
+    return lam, V, mu
+
+
+def suggest_size(m: int, lambda1: float, lambda2: float):
+    """Fig. 2 steps 2 and 5-15: (rows, cols, iterations) for m samples whose
+    two largest principal-component variances are lambda1 >= lambda2.
+    munits = ceil(5 sqrt(m)); r = sqrt(lambda1 / lambda2), or 1 when
+    lambda1 = 0 or lambda2 * munits < lambda1; size1 = the nearest integer to
+    sqrt(munits / (r sqrt(3/4))), within [1, munits]; size2 =
+    ceil(munits / size1); rows = min, cols = max; iterations =
+    ceil(50 rows cols / m) * m * 4."""
+    munits = int(np.ceil(5.0 * np.sqrt(m)))
+    if lambda1 == 0.0 or lambda2 * munits < lambda1:
+        r = 1.0
+    else:
+        r = float(np.sqrt(lambda1 / lambda2))
+    size1 = int(np.floor(np.sqrt(munits / (r * np.sqrt(0.75))) + 0.5))
+    size1 = max(1, min(munits, size1))
+    size2 = -(-munits // size1)
+    rows, cols = min(size1, size2), max(size1, size2)
+    iters = int(np.ceil(50.0 * rows * cols / m)) * m * 4
+    return rows, cols, iters
+
+
+def linear_init(mu: np.ndarray, lam, V: np.ndarray, rows: int, cols: int) -> np.ndarray:
+    """Sec. 6D: unit (r, c) starts at mu + a_c sqrt(lambda1) v1 +
+    b_r sqrt(lambda2) v2 with a_c = 2c/(cols-1) - 1 and b_r = 2r/(rows-1) - 1
+    (0 for a single column or row): the longer side of the map spans the
+    first component, the grid covering one standard deviation either side."""
+    W = np.empty((rows * cols, mu.size), dtype=np.float64)
+    s1, s2 = np.sqrt(max(lam[0], 0.0)), np.sqrt(max(lam[1], 0.0))
+    for r in range(rows):
+        b = 2.0 * r / (rows - 1) - 1.0 if rows > 1 else 0.0
+        for c in range(cols):
+            a = 2.0 * c / (cols - 1) - 1.0 if cols > 1 else 0.0
+            W[r * cols + c] = mu + a * s1 * V[:, 0] + b * s2 * V[:, 1]
+    return W

@@ -311,3 +311,76 @@ def test_argument_errors():
     W = np.zeros((4, 3))
     with pytest.raises(ValueError):
         oracle.train(W, 2, 2, X, np.array([5]), sched(0.1, 1.0))
+
+
+# ------------------------------------------------------------ linear init (Sec. 6D, Fig. 2)
+def _planar_data():
+    """Rows mu + 3 s_i e1 + t_i e4 with s, t two orthogonal +-1 patterns of
+    mean zero (Walsh rows of length 64): exactly representable, with
+    covariance 9 e1 e1^T + e4 e4^T."""
+    i = np.arange(64)
+    s = np.where((i & 1) == 0, 1.0, -1.0)
+    t = np.where((i & 2) == 0, 1.0, -1.0)
+    assert s.sum() == 0 and t.sum() == 0 and (s * t).sum() == 0
+    mu = np.array([1.0, 2.0, -3.0, 4.0, 0.5, 6.0])
+    X = mu + 3.0 * np.outer(s, np.eye(6)[1]) + np.outer(t, np.eye(6)[4])
+    return X.astype(np.float32), mu
+
+
+def test_pca_of_planar_data_recovers_its_axes():
+    X, mu = _planar_data()
+    lam, V, m = oracle.pca_top2(X)
+    assert np.allclose(lam, [9.0, 1.0], rtol=0, atol=1e-12)
+    assert np.allclose(V[:, 0], np.eye(6)[1], atol=1e-12)
+    assert np.allclose(V[:, 1], np.eye(6)[4], atol=1e-12)
+    assert np.array_equal(m, mu)
+
+
+def test_pca_sign_convention_and_definition():
+    rng = np.random.default_rng(3)
+    X = (rng.standard_normal((300, 12)) @ rng.standard_normal((12, 12))).astype(np.float32)
+    lam, V, mu = oracle.pca_top2(X)
+    Xc = X.astype(np.float64) - mu
+    Cov = Xc.T @ Xc / X.shape[0]
+    for a in range(2):
+        v = V[:, a]
+        assert abs(np.linalg.norm(v) - 1.0) < 1e-12
+        assert np.linalg.norm(Cov @ v - lam[a] * v) <= 1e-9 * lam[0]
+        k = int(np.argmax(np.abs(v)))
+        assert v[k] > 0
+    assert lam[0] >= lam[1] >= 0 and abs(V[:, 0] @ V[:, 1]) < 1e-12
+    # no direction has more variance than the first component
+    for u in rng.standard_normal((20, 12)):
+        u /= np.linalg.norm(u)
+        assert u @ Cov @ u <= lam[0] * (1 + 1e-12)
+
+
+def test_map_size_heuristic_by_hand():
+    # m = 100: munits = ceil(5 * 10) = 50.  lambda = (4, 1): 1 * 50 >= 4, so
+    # r = 2; sqrt(50 / (2 * 0.8660)) = 5.37 -> 5; ceil(50 / 5) = 10;
+    # iterations ceil(50 * 50 / 100) * 100 * 4 = 25 * 400.
+    assert oracle.suggest_size(100, 4.0, 1.0) == (5, 10, 10000)
+    # lambda1 > lambda2 * munits (and lambda1 = 0): r = 1;
+    # sqrt(50 / 0.8660) = 7.60 -> 8; ceil(50 / 8) = 7; ceil(50 * 56 / 100) = 28.
+    assert oracle.suggest_size(100, 1000.0, 1.0) == (7, 8, 11200)
+    assert oracle.suggest_size(100, 0.0, 0.0) == (7, 8, 11200)
+    # m = 2000: munits = ceil(223.6) = 224; r = sqrt(2);
+    # sqrt(224 / (1.4142 * 0.8660)) = 13.52 -> 14; ceil(224 / 14) = 16;
+    # ceil(50 * 224 / 2000) = ceil(5.6) = 6 -> 6 * 2000 * 4.
+    assert oracle.suggest_size(2000, 2.0, 1.0) == (14, 16, 48000)
+    # equal variances: r = 1 as in the second case
+    assert oracle.suggest_size(100, 1.0, 1.0) == (7, 8, 11200)
+
+
+def test_linear_init_spans_one_standard_deviation_per_component():
+    X, mu = _planar_data()
+    lam, V, m = oracle.pca_top2(X)
+    W = oracle.linear_init(m, lam, V, 3, 4)
+    e1, e4 = np.eye(6)[1], np.eye(6)[4]
+    assert np.allclose(W[0], mu - 3.0 * e1 - e4, atol=1e-12)
+    assert np.allclose(W[11], mu + 3.0 * e1 + e4, atol=1e-12)
+    for c, a in enumerate((-1.0, -1.0 / 3.0, 1.0 / 3.0, 1.0)):
+        assert np.allclose(W[4 + c], mu + 3.0 * a * e1, atol=1e-12)   # middle row
+    W1 = oracle.linear_init(m, lam, V, 1, 3)
+    assert np.allclose(W1[1], mu, atol=1e-12)                          # single row, centre
+    assert np.allclose(W1[0], mu - 3.0 * e1, atol=1e-12)
