@@ -180,6 +180,44 @@ som_status som_get_shape(const som_map *map, int32_t *rows, int32_t *cols,
  * `epoch` when no order is given (host int32 array of n entries). */
 som_status som_shuffle(uint64_t seed, int64_t epoch, int64_t n, int32_t *out);
 
+/* The two largest principal components of the n x d row-major fp32 device
+ * matrix X (paper Fig. 2 steps 3-4, Sec. 6D): eigenvalues lambda[0] >=
+ * lambda[1] of the covariance (1/n) sum_i (x_i - mu)(x_i - mu)^T into the
+ * host array lambda[2], and optionally the column means (mean) and the
+ * unit eigenvectors (v1, v2; sign such that the component of largest
+ * magnitude, lowest index on ties, is positive) into device arrays of d
+ * floats.  Computed on the device (fp32 matrix-core covariance, fp64-reduced
+ * subspace iteration until both residuals are below 2e-5 lambda[0], at most
+ * 4000 iterations) with d * d + 144 d floats of work memory allocated for
+ * the call; ordered on `stream` (a hipStream_t, NULL for the null stream),
+ * which it synchronizes.
+ * Errors: SOM_E_ARG (NULL X or lambda, n or d <= 0, pointers not covering
+ * their extent), SOM_E_OOM, SOM_E_DEVICE. */
+som_status som_pca2(const float *X, int64_t n, int32_t d, void *stream, double *lambda,
+                    float *mean, float *v1, float *v2);
+
+/* Map size and iteration count for m samples whose two largest
+ * principal-component variances are lambda1 >= lambda2 (paper Fig. 2):
+ * munits = ceil(5 sqrt(m)); r = sqrt(lambda1 / lambda2), or 1 when lambda1
+ * = 0 or lambda2 * munits < lambda1; size1 = the nearest integer to
+ * sqrt(munits / (r sqrt(3/4))) (the figure's garbled cube root read as the
+ * square root of 3/4, the hexagonal row pitch), within [1, munits]; size2 =
+ * ceil(munits / size1); rows = min(size1, size2), cols = max; iterations =
+ * ceil(50 rows cols / m) * m * 4.  Host arithmetic; outputs may be NULL.
+ * Errors: SOM_E_ARG (m <= 0, lambda2 < 0, lambda1 < lambda2, non-finite). */
+som_status som_suggest_size(int64_t m, double lambda1, double lambda2, int32_t *rows,
+                            int32_t *cols, int64_t *iterations);
+
+/* Linear initialisation (Sec. 6D): the map's prototypes become a regular
+ * grid in the plane through the mean mu of the n x d device matrix X spanned
+ * by its two largest principal components (as som_pca2):
+ *     w(r, c) = mu + a_c sqrt(lambda1) v1 + b_r sqrt(lambda2) v2,
+ *     a_c = 2c / (cols - 1) - 1,  b_r = 2r / (rows - 1) - 1   (0 for one
+ * column / row), so the longer side spans the first component over one
+ * standard deviation either side.  Synchronizes the map's stream.
+ * Errors: as som_pca2. */
+som_status som_init_linear(som_map *map, const float *X, int64_t n);
+
 /* Launch shape that som_train would use for this map: workgroups, threads
  * per workgroup and kernel variant (0 = prototypes streamed from memory once
  * per block of steps, 1 = prototypes held in LDS for the whole call, 2 / 3 =

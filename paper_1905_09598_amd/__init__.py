@@ -27,6 +27,7 @@ __all__ = [
     "som_train", "som_bmu", "som_bmu2", "som_quantization_error",
     "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
+    "som_pca2", "som_suggest_size", "som_init_linear",
     "som_status_string", "RECT", "HEX", "LINEAR", "EXPONENTIAL", "EXPORTED",
 ]
 
@@ -46,7 +47,7 @@ EXPORTED = (
     "som_train", "som_bmu", "som_bmu2", "som_quantization_error",
     "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
-    "som_status_string",
+    "som_pca2", "som_suggest_size", "som_init_linear", "som_status_string",
 )
 
 
@@ -106,6 +107,10 @@ def lib():
                           C.POINTER(i32)],
         "som_shuffle": [u64, i64, i64, vp],
         "som_train_plan": [vp, C.POINTER(i32), C.POINTER(i32), C.POINTER(i32)],
+        "som_pca2": [vp, i64, i32, vp, C.POINTER(C.c_double), vp, vp, vp],
+        "som_suggest_size": [i64, C.c_double, C.c_double, C.POINTER(i32), C.POINTER(i32),
+                             C.POINTER(i64)],
+        "som_init_linear": [vp, vp, i64],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -235,8 +240,38 @@ def som_train_plan(handle: int):
     return {"grid": g.value, "block": b.value, "variant": v.value}
 
 
+def som_pca2(X, n: int, d: int, stream=None, mean=None, v1=None, v2=None):
+    """Two largest covariance eigenvalues of X (host floats); the means and
+    unit eigenvectors go to the optional device arrays."""
+    lam = (C.c_double * 2)()
+    _check(lib().som_pca2(_ptr(X), n, d, stream, lam, _ptr(mean), _ptr(v1), _ptr(v2)),
+           "som_pca2")
+    return lam[0], lam[1]
+
+
+def som_suggest_size(m: int, lambda1: float, lambda2: float):
+    r, c, t = C.c_int32(), C.c_int32(), C.c_int64()
+    _check(lib().som_suggest_size(m, lambda1, lambda2, C.byref(r), C.byref(c), C.byref(t)),
+           "som_suggest_size")
+    return r.value, c.value, t.value
+
+
+def som_init_linear(handle: int, X, n: int) -> None:
+    _check(lib().som_init_linear(handle, _ptr(X), n), "som_init_linear")
+
+
 def som_status_string(code: int) -> str:
     return lib().som_status_string(code).decode()
+
+
+def pca2(X):
+    """(lambda1, lambda2, mean, v1, v2) of the rows of the device matrix X."""
+    import torch
+    _require(X, "float32", "X")
+    n, d = X.shape
+    mean, v1, v2 = (torch.empty(d, dtype=torch.float32, device=X.device) for _ in range(3))
+    l1, l2 = som_pca2(X, n, d, _current_stream(), mean, v1, v2)
+    return l1, l2, mean, v1, v2
 
 
 # ---------------------------------------------------------------- wrapper
@@ -343,3 +378,9 @@ class Map:
 
     def plan(self) -> dict:
         return som_train_plan(self.handle)
+
+    def init_linear(self, X) -> None:
+        """Prototypes on the plane of X's two largest principal components."""
+        _require(X, "float32", "X")
+        self._bind_stream()
+        som_init_linear(self.handle, X, X.shape[0])

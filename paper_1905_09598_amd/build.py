@@ -20,7 +20,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libsom.so")
-SOURCES = ["som_api.cpp", "som_train.hip", "som_train_pipe.hip", "som_eval.hip", "som_util.hip"]
+SOURCES = ["som_api.cpp", "som_train.hip", "som_train_pipe.hip", "som_eval.hip", "som_util.hip",
+           "som_pca.hip"]
 ARCH = "gfx950"
 
 

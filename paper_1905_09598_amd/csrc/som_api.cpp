@@ -14,6 +14,11 @@
 
 #include <vector>
 
+// Subspace iteration of the principal components: residual target relative
+// to the largest eigenvalue, and an iteration cap.
+static constexpr int kPcaMaxIters = 4000;
+static constexpr double kPcaTol = 2e-5;
+
 struct som_map {
     int32_t rows = 0, cols = 0, d = 0, topology = SOM_RECT;
     int32_t N = 0;
@@ -340,6 +345,91 @@ static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
     if (a.variant < 0 || a.variant > 5) a.variant = 0;
     a.timeout_ticks = 100000000ull * 20;  // 20 s at the 100 MHz reference clock
     return a;
+}
+
+// Principal components on the device; the vectors stay in *work (freed by
+// the caller with hipFree).
+static som_status pca_run(const float *X, int64_t n, int32_t d, hipStream_t stream,
+                          double *lambda, float **work, float **mean) {
+    *work = nullptr;
+    *mean = nullptr;
+    double *stats = nullptr;
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(work), som::pca_work_floats(d) * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(mean), (size_t)d * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&stats), 4 * sizeof(double));
+    if (e == hipSuccess)
+        e = som::pca_top2(X, n, d, *work, *mean, stats, kPcaMaxIters, kPcaTol, stream, lambda,
+                          nullptr);
+    (void)hipFree(stats);
+    if (e != hipSuccess) {
+        (void)hipFree(*work);
+        (void)hipFree(*mean);
+        *work = nullptr;
+        *mean = nullptr;
+        return from_hip(e);
+    }
+    return SOM_OK;
+}
+
+som_status som_pca2(const float *X, int64_t n, int32_t d, void *stream, double *lambda,
+                    float *mean, float *v1, float *v2) {
+    if (!X || !lambda || n <= 0 || d <= 0 || n > INT32_MAX) return SOM_E_ARG;
+    if (!device_range_ok(X, (uint64_t)n * (uint64_t)d * sizeof(float))) return SOM_E_ARG;
+    for (float *p : {mean, v1, v2})
+        if (p && !device_range_ok(p, (uint64_t)d * sizeof(float))) return SOM_E_ARG;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    float *work = nullptr, *mu = nullptr;
+    som_status st = pca_run(X, n, d, s, lambda, &work, &mu);
+    if (st != SOM_OK) return st;
+    const float *V = som::pca_vectors(work, d);
+    hipError_t e = hipSuccess;
+    if (mean) e = hipMemcpyAsync(mean, mu, (size_t)d * 4, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && v1) e = hipMemcpyAsync(v1, V, (size_t)d * 4, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && v2)
+        e = hipMemcpyAsync(v2, V + d, (size_t)d * 4, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    (void)hipFree(work);
+    (void)hipFree(mu);
+    return from_hip(e);
+}
+
+som_status som_suggest_size(int64_t m, double lambda1, double lambda2, int32_t *rows,
+                            int32_t *cols, int64_t *iterations) {
+    if (m <= 0 || !(lambda1 >= 0.0) || !(lambda2 >= 0.0) || lambda2 > lambda1 ||
+        !isfinite(lambda1))
+        return SOM_E_ARG;
+    // Fig. 2: munits units, side ratio from the two largest variances.
+    const double munits = ceil(5.0 * sqrt((double)m));
+    if (munits > (double)INT32_MAX) return SOM_E_ARG;
+    const double r = (lambda1 == 0.0 || lambda2 * munits < lambda1) ? 1.0 : sqrt(lambda1 / lambda2);
+    double size1 = floor(sqrt(munits / (r * sqrt(0.75))) + 0.5);
+    if (size1 < 1.0) size1 = 1.0;
+    if (size1 > munits) size1 = munits;
+    const double size2 = ceil(munits / size1);
+    const double nr = size1 < size2 ? size1 : size2, nc = size1 < size2 ? size2 : size1;
+    const double iters = ceil(50.0 * nr * nc / (double)m) * (double)m * 4.0;
+    if (iters > 9.2e18) return SOM_E_ARG;
+    if (rows) *rows = (int32_t)nr;
+    if (cols) *cols = (int32_t)nc;
+    if (iterations) *iterations = (int64_t)iters;
+    return SOM_OK;
+}
+
+som_status som_init_linear(som_map *m, const float *X, int64_t n) {
+    if (!m || !X || n <= 0 || n > INT32_MAX) return SOM_E_ARG;
+    if (!device_range_ok(X, (uint64_t)n * (uint64_t)m->d * sizeof(float))) return SOM_E_ARG;
+    double lambda[2];
+    float *work = nullptr, *mu = nullptr;
+    som_status st = pca_run(X, n, m->d, m->stream, lambda, &work, &mu);
+    if (st != SOM_OK) return st;
+    const float *V = som::pca_vectors(work, m->d);
+    hipError_t e = som::launch_linear_init(m->W, m->ld, m->rows, m->cols, m->d, mu, V, V + m->d,
+                                           lambda[0], lambda[1], m->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+    (void)hipFree(work);
+    (void)hipFree(mu);
+    if (e != hipSuccess) return from_hip(e);
+    return check_deferred(m);
 }
 
 som_status som_train_plan(const som_map *m, int32_t *grid, int32_t *block,

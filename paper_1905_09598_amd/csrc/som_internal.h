@@ -133,4 +133,21 @@ hipError_t launch_qe_te_reduce(const int32_t *idx1, const int32_t *idx2,
                                const float *d1, int64_t n, int32_t cols,
                                int32_t topology, double *out2, hipStream_t s);
 
+// Principal components and linear initialisation (som_pca.hip).
+constexpr int kPcaBlock = 8;  // subspace-iteration block
+// Floats of work memory for pca_top2 (covariance d x d, iteration vectors,
+// column partial sums).
+size_t pca_work_floats(int32_t d);
+// Two largest eigenvalues of the covariance of the n x d rows of X (host
+// lambda[2]) and the column means (mean, d floats); the unit eigenvectors
+// are left in pca_vectors(work, d) (columns 0 and 1, stride d).  stats: 4
+// device doubles.  Iterates until both residuals are below tol * lambda1
+// or max_iters; synchronizes the stream.
+hipError_t pca_top2(const float *X, int64_t n, int32_t d, float *work, float *mean, double *stats,
+                    int max_iters, double tol, hipStream_t s, double *lambda, int *iters);
+const float *pca_vectors(const float *work, int32_t d);
+hipError_t launch_linear_init(float *W, int64_t ld, int32_t rows, int32_t cols, int32_t d,
+                              const float *mean, const float *v1, const float *v2, double lambda1,
+                              double lambda2, hipStream_t s);
+
 }  // namespace som

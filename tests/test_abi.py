@@ -77,3 +77,30 @@ def test_library_shuffle_matches_independent_oracle_shuffle(seed, epoch, n):
     lib_perm = som.som_shuffle(seed, epoch, n)
     assert np.array_equal(lib_perm, oracle.shuffle(seed, epoch, n))
     assert sorted(lib_perm.tolist()) == list(range(n))
+
+
+def test_library_size_heuristic_equals_independent_oracle():
+    rng = np.random.default_rng(5)
+    cases = [(100, 4.0, 1.0), (100, 1000.0, 1.0), (100, 0.0, 0.0), (2000, 2.0, 1.0),
+             (1, 1.0, 1.0), (637, 3.7, 1.2)]
+    for _ in range(200):
+        m = int(rng.integers(1, 200000))
+        l1 = float(rng.uniform(0.0, 10.0))
+        cases.append((m, l1, float(rng.uniform(0.0, l1))))
+    for m, l1, l2 in cases:
+        assert som.som_suggest_size(m, l1, l2) == oracle.suggest_size(m, l1, l2), (m, l1, l2)
+
+
+def test_pca_and_linear_init_argument_errors():
+    L = som.lib()
+    lam = (C.c_double * 2)()
+    assert L.som_pca2(None, 10, 4, None, lam, None, None, None) == 1
+    assert L.som_pca2(1, 0, 4, None, lam, None, None, None) == 1
+    assert L.som_pca2(1, 10, 0, None, lam, None, None, None) == 1
+    assert L.som_pca2(1, 10, 4, None, None, None, None, None) == 1
+    assert L.som_init_linear(None, 1, 10) == 1
+    r = C.c_int32()
+    assert L.som_suggest_size(0, 1.0, 1.0, C.byref(r), None, None) == 1
+    assert L.som_suggest_size(10, 1.0, 2.0, C.byref(r), None, None) == 1
+    assert L.som_suggest_size(10, -1.0, -2.0, C.byref(r), None, None) == 1
+    assert L.som_suggest_size(10, float("nan"), 0.0, C.byref(r), None, None) == 1
