@@ -98,9 +98,9 @@ typedef struct som_map som_map;
 
 /* Create a rows x cols map of d-dimensional fp32 prototypes on the current
  * HIP device and initialise them U[0,1): element i = u * d + j is the top
- * 24 bits of the i-th SplitMix64 output of `seed`, times 2^-24 (the paper
- * initialises on the principal-component plane, Sec. 6D; that is not built
- * here).  The prototypes are owned by the map.  Topology starts as RECT and
+ * 24 bits of the i-th SplitMix64 output of `seed`, times 2^-24 (the paper's
+ * principal-component plane initialisation, Sec. 6D, is som_init_linear).
+ * The prototypes are owned by the map.  Topology starts as RECT and
  * the stream as the null stream.
  * Errors: SOM_E_ARG (rows, cols or d <= 0, rows * cols > 2^24 - 1,
  * rows * cols * d overflows, out == NULL), SOM_E_OOM, SOM_E_DEVICE.
@@ -136,6 +136,35 @@ som_status som_set_stream(som_map *map, void *stream);
  * reported as SOM_E_BAD_ORDER by the next synchronizing call. */
 som_status som_train(som_map *map, const float *X, int64_t n, int32_t epochs,
                      const som_schedule *sched);
+
+/* Online training from sparse samples: the same steps as som_train (Eq. (1)
+ * of Sec. 5A, one BMU per step, lowest index on ties) for the n rows of a
+ * CSR matrix, such as the L2-normalised TF-IDF vectors of Sec. 6B, at a
+ * cost per step proportional to the row's non-zeros rather than to d.
+ *   indptr   device int64 array of n + 1 offsets, indptr[0] = 0; row i is
+ *            entries indptr[i] .. indptr[i+1] - 1 of indices and values.
+ *   indices  device int32 array of indptr[n] feature indices, strictly
+ *            increasing within each row, in [0, d).
+ *   values   device fp32 array of indptr[n] values.
+ * indices and values may be NULL when indptr[n] = 0.  The schedule fields
+ * mean what they mean for som_train.
+ * Internally each prototype is held as a scale times an fp64 vector stored
+ * feature by feature ((d + 3) * roundup(rows * cols, 64) doubles, plus
+ * 12 * K + 16 bytes per step for the padded entries, K = 16, 32 or 64 from
+ * the longest row; both kept by the map for later calls), so a step reads
+ * and writes only the sample's features; distances are evaluated in fp64
+ * and rounded once to fp32 for the BMU comparison.  The call synchronizes
+ * the stream twice to validate the CSR structure before training, which is
+ * then stream-ordered.
+ * Errors: as som_train, and SOM_E_ARG (indptr NULL or not covering n + 1
+ * entries, indptr[0] != 0, a row with decreasing offsets or offsets past
+ * indptr[n], indices not strictly increasing within a row or outside
+ * [0, d), indices or values not covering indptr[n] entries),
+ * SOM_E_UNSUPPORTED (a row with more than 64 non-zeros, or more than 16,384
+ * units), SOM_E_OOM (the buffers above beyond the map's memory cap). */
+som_status som_train_csr(som_map *map, const int64_t *indptr, const int32_t *indices,
+                         const float *values, int64_t n, int32_t epochs,
+                         const som_schedule *sched);
 
 /* Batched BMU assignment (Sec. 8A): for each of the n rows of the device
  * matrix X, out_idx[i] = BMU index (lowest index among equal minima).

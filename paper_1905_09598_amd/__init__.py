@@ -24,7 +24,7 @@ from typing import Optional
 __all__ = [
     "SomError", "LibraryMissing", "Schedule", "Map", "lib", "library_path",
     "som_create", "som_destroy", "som_set_topology", "som_set_stream",
-    "som_train", "som_bmu", "som_bmu2", "som_quantization_error",
+    "som_train", "som_train_csr", "som_bmu", "som_bmu2", "som_quantization_error",
     "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
     "som_pca2", "som_suggest_size", "som_init_linear",
@@ -44,7 +44,7 @@ STATUS = {0: "SOM_OK", 1: "SOM_E_ARG", 2: "SOM_E_OOM", 3: "SOM_E_DEVICE",
 # Every symbol include/som.h declares.
 EXPORTED = (
     "som_create", "som_destroy", "som_set_topology", "som_set_stream",
-    "som_train", "som_bmu", "som_bmu2", "som_quantization_error",
+    "som_train", "som_train_csr", "som_bmu", "som_bmu2", "som_quantization_error",
     "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
     "som_pca2", "som_suggest_size", "som_init_linear", "som_status_string",
@@ -96,6 +96,7 @@ def lib():
         "som_set_topology": [vp, i32],
         "som_set_stream": [vp, vp],
         "som_train": [vp, vp, i64, i32, C.POINTER(Schedule)],
+        "som_train_csr": [vp, vp, vp, vp, i64, i32, C.POINTER(Schedule)],
         "som_bmu": [vp, vp, i64, vp],
         "som_bmu2": [vp, vp, i64, vp, vp, vp],
         "som_quantization_error": [vp, vp, i64, C.POINTER(C.c_double)],
@@ -182,6 +183,12 @@ def som_set_stream(handle: int, stream: Optional[int]) -> None:
 
 def som_train(handle: int, X, n: int, epochs: int, sched: Schedule) -> None:
     _check(lib().som_train(handle, _ptr(X), n, epochs, C.byref(sched)), "som_train")
+
+
+def som_train_csr(handle: int, indptr, indices, values, n: int, epochs: int,
+                  sched: Schedule) -> None:
+    _check(lib().som_train_csr(handle, _ptr(indptr), _ptr(indices), _ptr(values), n, epochs,
+                               C.byref(sched)), "som_train_csr")
 
 
 def som_bmu(handle: int, X, n: int, out_idx) -> None:
@@ -330,6 +337,31 @@ class Map:
                           shuffle_seed, order, step0, total_steps, bmu_trace)
         self._bind_stream()
         som_train(self.handle, X, X.shape[0], int(epochs), s)
+
+    def train_csr(self, indptr, indices, values, epochs: int, lr0: float, lr1: float,
+                  sigma0: float, sigma1: float, lr_decay: int = LINEAR,
+                  sigma_decay: int = EXPONENTIAL, order=None, shuffle_seed: int = 0,
+                  step0: int = 0, total_steps: int = 0, bmu_trace=None) -> None:
+        """Train from the n rows of a CSR matrix (int64 indptr of n + 1
+        offsets, int32 column indices sorted within each row, fp32 values,
+        all on the GPU)."""
+        _require(indptr, "int64", "indptr")
+        _require(indices, "int32", "indices")
+        _require(values, "float32", "values")
+        if indptr.dim() != 1 or indptr.numel() < 2:
+            raise ValueError("indptr must be 1-D with n + 1 entries")
+        if indices.numel() != values.numel():
+            raise ValueError("indices and values must have the same length")
+        if order is not None:
+            _require(order, "int32", "order")
+        if bmu_trace is not None:
+            _require(bmu_trace, "int32", "bmu_trace")
+        s = make_schedule(lr0, lr1, sigma0, sigma1, lr_decay, sigma_decay,
+                          shuffle_seed, order, step0, total_steps, bmu_trace)
+        self._bind_stream()
+        nnz = indices.numel()
+        som_train_csr(self.handle, indptr, indices if nnz else None, values if nnz else None,
+                      indptr.numel() - 1, int(epochs), s)
 
     def bmu(self, X, second: bool = False):
         _require(X, "float32", "X")

@@ -44,6 +44,14 @@ struct som_map {
     // when d % 4 != 0 or X is not 16-byte aligned)
     float *xpad = nullptr;
     int64_t xpad_cap = 0;
+    // sparse training: feature-major fp64 prototypes with their scales and
+    // norms ((d + 1) * ldv + 2 * ldv doubles) and the per-step entries
+    double *sv = nullptr;
+    int64_t sv_cap = 0;
+    int32_t *sidx = nullptr;
+    float *sval = nullptr, *spv = nullptr;
+    double2 *sxs = nullptr;
+    int64_t sidx_cap = 0, sval_cap = 0, spv_cap = 0, sxs_cap = 0;
     // evaluation scratch
     float *wnorm = nullptr;
     int32_t *cand = nullptr, *idx1 = nullptr, *idx2 = nullptr;
@@ -141,6 +149,20 @@ som_status grow(T **p, int64_t count) {
         if (e != hipSuccess) return from_hip(e);
     }
     return from_hip(hipMalloc(reinterpret_cast<void **>(p), (size_t)count * sizeof(T)));
+}
+
+// Make *p hold at least `need` elements (waiting for the stream before a
+// buffer it may still use is replaced).
+template <typename T>
+hipError_t ensure(som_map *m, T **p, int64_t *cap, int64_t need) {
+    if (*cap >= need) return hipSuccess;
+    hipError_t e = hipStreamSynchronize(m->stream);
+    if (e == hipSuccess && *p) e = hipFree(*p);
+    *p = nullptr;
+    *cap = 0;
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(p), (size_t)need * sizeof(T));
+    if (e == hipSuccess) *cap = need;
+    return e;
 }
 
 som_status ensure_eval_scratch(som_map *m, int64_t n, int64_t ncand) {
@@ -286,6 +308,11 @@ som_status som_destroy(som_map *m) {
     (void)hipFree(m->sched);
     (void)hipFree(m->block_dots);
     (void)hipFree(m->xpad);
+    (void)hipFree(m->sv);
+    (void)hipFree(m->sidx);
+    (void)hipFree(m->sval);
+    (void)hipFree(m->spv);
+    (void)hipFree(m->sxs);
     (void)hipFree(m->wnorm);
     (void)hipFree(m->cand);
     (void)hipFree(m->idx1);
@@ -446,27 +473,12 @@ som_status som_train_plan(const som_map *m, int32_t *grid, int32_t *block,
     return SOM_OK;
 }
 
-som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
-                     const som_schedule *s) {
-    if (!m || !X || !s || n <= 0 || epochs <= 0) return SOM_E_ARG;
-    if (n > INT32_MAX || (int64_t)epochs * n > INT32_MAX) return SOM_E_ARG;
-    if (!schedule_ok(s)) return SOM_E_ARG;
-    const int64_t nsteps = (int64_t)epochs * n;
-    if (s->step0 < 0) return SOM_E_ARG;
-    const int64_t total = s->total_steps == 0 ? s->step0 + nsteps : s->total_steps;
-    if (total < s->step0 + nsteps) return SOM_E_ARG;
-    if (!device_range_ok(X, (uint64_t)n * (uint64_t)m->d * sizeof(float))) return SOM_E_ARG;
-    if (s->order && !device_range_ok(s->order, (uint64_t)nsteps * sizeof(int32_t)))
-        return SOM_E_ARG;
-    if (s->bmu_trace && !device_range_ok(s->bmu_trace, (uint64_t)nsteps * sizeof(int32_t)))
-        return SOM_E_ARG;
-
-    som::TrainArgs a = train_args(m, X, n);
-    som::TrainPlan plan;
-    hipError_t e = som::plan_train(a, m->num_cus, &plan);
-    if (e == hipErrorInvalidValue) return SOM_E_UNSUPPORTED;
-    if (e != hipSuccess) return from_hip(e);
-
+// The per-step inputs of a training call: the sample order (the library's
+// shuffle when the schedule gives none, staged through pinned memory) and
+// the schedule table; fills a's order, step and schedule fields.
+static hipError_t stage_steps(som_map *m, const som_schedule *s, int64_t n, int64_t nsteps,
+                              int64_t total, som::TrainArgs &a) {
+    hipError_t e;
     const int32_t *order = s->order;
     if (!order) {
         // Library order: epoch e = t / n presents permutation e of [0, n).
@@ -482,11 +494,11 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
             if (e == hipSuccess)
                 e = hipHostMalloc(reinterpret_cast<void **>(&m->order_host), (size_t)nsteps * 4,
                                   hipHostMallocDefault);
-            if (e != hipSuccess) return from_hip(e);
+            if (e != hipSuccess) return e;
             m->order_cap = nsteps;
         }
         e = hipEventSynchronize(m->order_done);  // previous upload has left the buffer
-        if (e != hipSuccess) return from_hip(e);
+        if (e != hipSuccess) return e;
         std::vector<int32_t> perm((size_t)n);
         int64_t cur_epoch = -1;
         for (int64_t k = 0; k < nsteps; ++k) {
@@ -501,7 +513,7 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
         e = hipMemcpyAsync(m->order_dev, m->order_host, (size_t)nsteps * 4,
                            hipMemcpyHostToDevice, m->stream);
         if (e == hipSuccess) e = hipEventRecord(m->order_done, m->stream);
-        if (e != hipSuccess) return from_hip(e);
+        if (e != hipSuccess) return e;
         order = m->order_dev;
     }
 
@@ -523,10 +535,45 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
         m->sched_cap = 0;
         if (e == hipSuccess)
             e = hipMalloc(reinterpret_cast<void **>(&m->sched), (size_t)nsteps * sizeof(float2));
-        if (e != hipSuccess) return from_hip(e);
+        if (e != hipSuccess) return e;
         m->sched_cap = nsteps;
     }
     a.sched = m->sched;
+    return hipSuccess;
+}
+
+// Checks shared by the training calls: step counts, schedule, order and
+// trace extents.  Sets the call's step count and schedule length.
+static bool train_call_ok(const som_schedule *s, int64_t n, int32_t epochs, int64_t *nsteps,
+                          int64_t *total) {
+    if (!s || n <= 0 || epochs <= 0) return false;
+    if (n > INT32_MAX || (int64_t)epochs * n > INT32_MAX) return false;
+    if (!schedule_ok(s)) return false;
+    *nsteps = (int64_t)epochs * n;
+    if (s->step0 < 0) return false;
+    *total = s->total_steps == 0 ? s->step0 + *nsteps : s->total_steps;
+    if (*total < s->step0 + *nsteps) return false;
+    if (s->order && !device_range_ok(s->order, (uint64_t)*nsteps * sizeof(int32_t)))
+        return false;
+    if (s->bmu_trace && !device_range_ok(s->bmu_trace, (uint64_t)*nsteps * sizeof(int32_t)))
+        return false;
+    return true;
+}
+
+som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
+                     const som_schedule *s) {
+    int64_t nsteps = 0, total = 0;
+    if (!m || !X || !train_call_ok(s, n, epochs, &nsteps, &total)) return SOM_E_ARG;
+    if (!device_range_ok(X, (uint64_t)n * (uint64_t)m->d * sizeof(float))) return SOM_E_ARG;
+
+    som::TrainArgs a = train_args(m, X, n);
+    som::TrainPlan plan;
+    hipError_t e = som::plan_train(a, m->num_cus, &plan);
+    if (e == hipErrorInvalidValue) return SOM_E_UNSUPPORTED;
+    if (e != hipSuccess) return from_hip(e);
+
+    e = stage_steps(m, s, n, nsteps, total, a);
+    if (e != hipSuccess) return from_hip(e);
     if (plan.variant >= 2) {
         const int64_t need = som::pipe_block_dots_floats(plan.block_m, nsteps);
         if (m->block_dots_cap < need) {
@@ -563,6 +610,70 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
     a.slot_spread = plan.slot_spread;
     e = som::launch_prepare_train(a, m->sched, m->stream);
     if (e == hipSuccess) e = som::launch_train(a, plan, m->stream);
+    return from_hip(e);
+}
+
+som_status som_train_csr(som_map *m, const int64_t *indptr, const int32_t *indices,
+                         const float *values, int64_t n, int32_t epochs, const som_schedule *s) {
+    int64_t nsteps = 0, total = 0;
+    if (!m || !indptr || !train_call_ok(s, n, epochs, &nsteps, &total)) return SOM_E_ARG;
+    if (!device_range_ok(indptr, (uint64_t)(n + 1) * sizeof(int64_t))) return SOM_E_ARG;
+    const int64_t ldv = ((int64_t)m->N + 63) & ~(int64_t)63;
+    if (ldv / 64 > som::kSparseMaxGrid) return SOM_E_UNSUPPORTED;
+
+    // The CSR structure: indptr[0] = 0, nnz = indptr[n], then every row on
+    // the device (lengths, sorted unique indices in [0, d), longest row).
+    int64_t ends[2] = {-1, -1};
+    hipError_t e = hipMemcpyAsync(&ends[0], indptr, sizeof(int64_t), hipMemcpyDeviceToHost, m->stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(&ends[1], indptr + n, sizeof(int64_t), hipMemcpyDeviceToHost,
+                           m->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+    if (e != hipSuccess) return from_hip(e);
+    if (ends[0] != 0 || ends[1] < 0) return SOM_E_ARG;
+    const int64_t nnz = ends[1];
+    if (nnz > 0 && (!device_range_ok(indices, (uint64_t)nnz * sizeof(int32_t)) ||
+                    !device_range_ok(values, (uint64_t)nnz * sizeof(float))))
+        return SOM_E_ARG;
+    e = som::launch_csr_check(indptr, indices, n, nnz, m->d, m->state, m->stream);
+    som::DevState st{};
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(&st, m->state, sizeof(st), hipMemcpyDeviceToHost, m->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(m->stream);
+    if (e != hipSuccess) return from_hip(e);
+    if (st.csr_bad) return SOM_E_ARG;
+    if (st.csr_max_len > som::kSparseMaxNnz) return SOM_E_UNSUPPORTED;
+    const int K = st.csr_max_len <= 16 ? 16 : st.csr_max_len <= 32 ? 32 : 64;
+
+    som::TrainArgs a = train_args(m, nullptr, n);
+    a.grid = (int32_t)(ldv / 64);
+    a.slot_spread = a.grid <= 64 ? 16 : 4;
+    const uint64_t vbytes = ((uint64_t)m->d + 3) * (uint64_t)ldv * sizeof(double);
+    const uint64_t ebytes = (uint64_t)nsteps * (uint64_t)K * 12 + (uint64_t)nsteps * 16;
+    if (vbytes + ebytes > max_bytes()) return SOM_E_OOM;
+    e = stage_steps(m, s, n, nsteps, total, a);
+    if (e == hipSuccess) e = ensure(m, &m->sv, &m->sv_cap, ((int64_t)m->d + 3) * ldv);
+    if (e == hipSuccess) e = ensure(m, &m->sidx, &m->sidx_cap, nsteps * K);
+    if (e == hipSuccess) e = ensure(m, &m->sval, &m->sval_cap, nsteps * K);
+    if (e == hipSuccess) e = ensure(m, &m->spv, &m->spv_cap, nsteps * K);
+    if (e == hipSuccess) e = ensure(m, &m->sxs, &m->sxs_cap, nsteps);
+    if (e != hipSuccess) return from_hip(e);
+
+    som::SparseArgs sp{};
+    sp.V = m->sv;
+    sp.ldv = ldv;
+    sp.S = m->sv + ((int64_t)m->d + 1) * ldv;
+    sp.WW = sp.S + ldv;
+    sp.K = K;
+    sp.sidx = m->sidx;
+    sp.sval = m->sval;
+    sp.spv = m->spv;
+    sp.sxs = m->sxs;
+    e = som::launch_prepare_train(a, m->sched, m->stream);
+    if (e == hipSuccess) e = som::launch_sparse_steps(a, sp, indptr, indices, values, m->stream);
+    if (e == hipSuccess) e = som::launch_sparse_enter(a, sp, m->stream);
+    if (e == hipSuccess) e = som::launch_train_sparse(a, sp, m->stream);
+    if (e == hipSuccess) e = som::launch_sparse_leave(a, sp, m->stream);
     return from_hip(e);
 }
 

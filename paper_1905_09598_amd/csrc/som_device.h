@@ -245,11 +245,11 @@ struct Bcast {
 };
 
 // One wave per workgroup: publish this workgroup's best key to grid
-// exchange number e and return the winning unit over every workgroup's slot
-// (the same in all lanes), or -1 if the wait was given up.
-__device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long best) {
+// exchange number e (the two halves of exchange() below, for callers that
+// work between them).
+__device__ inline void exchange_publish(const TrainArgs &a, int64_t e, unsigned long long best) {
     const int lane = threadIdx.x & 63, G = a.grid;
-    if (G == 1) return (int)(best & (unsigned long long)kMaxUnits);
+    if (G == 1) return;
     const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
     const int sp = a.slot_spread;
     const int64_t par = (e & 1) * (int64_t)G * sp;
@@ -260,6 +260,17 @@ __device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long
         __hip_atomic_store(a.slots + lane * kSlotReplicaStride + par + (int64_t)blockIdx.x * sp,
                            v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+}
+
+// Wait for every workgroup's key of exchange e and return the winning unit
+// (the same in all lanes), or -1 if the wait was given up.  `best` is this
+// workgroup's own key (the answer when the grid is one workgroup).
+__device__ inline int exchange_wait(const TrainArgs &a, int64_t e, unsigned long long best) {
+    const int lane = threadIdx.x & 63, G = a.grid;
+    if (G == 1) return (int)(best & (unsigned long long)kMaxUnits);
+    const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
+    const int sp = a.slot_spread;
+    const int64_t par = (e & 1) * (int64_t)G * sp;
     const unsigned long long *slots =
         a.slots + (blockIdx.x % kSlotReplicas) * kSlotReplicaStride + par;
     unsigned long long m = ~0ull;
@@ -294,6 +305,16 @@ __device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long
     m = wave_min_key(m, G <= 64);
     if (__ballot(abort) != 0) return -1;
     return (int)(m & (unsigned long long)kMaxUnits);
+}
+
+// Publish this workgroup's best key to grid exchange number e and return
+// the winning unit over every workgroup's slot, or -1 if the wait was given
+// up.  Each workgroup writes its key into every XCD's copy of the slot
+// array and polls the copy of its own XCD; slots alternate by the parity
+// of e and carry a tag of e, so a slot is never read for the wrong step.
+__device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long best) {
+    exchange_publish(a, e, best);
+    return exchange_wait(a, e, best);
 }
 
 // Neighbourhood factor of owned row r given BMU c: lr * 2^(-g * c2) with g

@@ -25,7 +25,8 @@ constexpr int64_t kSlotWords = kSlotReplicas * kSlotReplicaStride;
 struct DevState {
     int32_t status;     // sticky error code (som_status), cleared by the host
     int32_t order_bad;  // 1 if the current call's order has an index outside [0, n)
-    int32_t pad[2];
+    int32_t csr_bad;    // 1 if the current call's CSR rows are malformed
+    int32_t csr_max_len;  // longest CSR row of the current call
 };
 
 struct TrainArgs {
@@ -132,6 +133,35 @@ hipError_t launch_bmu_rerank(const EvalArgs &a, hipStream_t s);
 hipError_t launch_qe_te_reduce(const int32_t *idx1, const int32_t *idx2,
                                const float *d1, int64_t n, int32_t cols,
                                int32_t topology, double *out2, hipStream_t s);
+
+// Sparse-input training (som_sparse.hip).  Prototypes are held as
+// w_u = S_u v_u with v stored feature-major in fp64, V[j * ldv + u], so a
+// step touches only the rows of V at the sample's non-zero features.  Row d
+// of V is a scratch row that the padding entries of a step point to.
+constexpr int kSparseMaxNnz = 64;      // non-zeros per sample row
+constexpr int kSparseMaxGrid = 256;    // workgroups of 64 units
+struct SparseArgs {
+    double *V;            // (d + 1) x ldv
+    int64_t ldv;          // units rounded up to a multiple of 64
+    double *S;            // ldv scales
+    double *WW;           // ldv squared prototype norms |w_u|^2
+    int32_t K;            // entries per step: 16, 32 or 64
+    int32_t *sidx;        // nsteps x K feature indices (d for padding)
+    float *sval;          // nsteps x K values (0 for padding)
+    float *spv;           // nsteps x K: the previous step's sample at sidx
+    double2 *sxs;         // nsteps x (|x_s|^2, x_{s-1} . x_s)
+};
+// Per CSR row: lengths, sorted unique indices in [0, d); raises csr_bad and
+// records the longest row in csr_max_len (both zeroed first).
+hipError_t launch_csr_check(const int64_t *indptr, const int32_t *indices, int64_t n,
+                            int64_t nnz, int32_t d, DevState *state, hipStream_t s);
+// Per-step entries of the call's steps from the CSR rows and the order.
+hipError_t launch_sparse_steps(const TrainArgs &a, const SparseArgs &sp, const int64_t *indptr,
+                               const int32_t *indices, const float *values, hipStream_t s);
+// W (N x ld fp32) into V, S = 1, WW = |w|^2, and back: W = S v.
+hipError_t launch_sparse_enter(const TrainArgs &a, const SparseArgs &sp, hipStream_t s);
+hipError_t launch_sparse_leave(const TrainArgs &a, const SparseArgs &sp, hipStream_t s);
+hipError_t launch_train_sparse(const TrainArgs &a, const SparseArgs &sp, hipStream_t s);
 
 // Principal components and linear initialisation (som_pca.hip).
 constexpr int kPcaBlock = 8;  // subspace-iteration block
