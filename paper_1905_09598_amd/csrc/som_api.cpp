@@ -48,10 +48,10 @@ struct som_map {
     // norms ((d + 1) * ldv + 2 * ldv doubles) and the per-step entries
     double *sv = nullptr;
     int64_t sv_cap = 0;
-    int32_t *sidx = nullptr;
-    float *sval = nullptr, *spv = nullptr;
-    double2 *sxs = nullptr;
-    int64_t sidx_cap = 0, sval_cap = 0, spv_cap = 0, sxs_cap = 0;
+    uint32_t *soff = nullptr;
+    double *sval = nullptr, *spv1 = nullptr, *spv2 = nullptr;
+    som::SparseStep *sst = nullptr;
+    int64_t soff_cap = 0, sval_cap = 0, spv1_cap = 0, spv2_cap = 0, sst_cap = 0;
     // evaluation scratch
     float *wnorm = nullptr;
     int32_t *cand = nullptr, *idx1 = nullptr, *idx2 = nullptr;
@@ -309,10 +309,11 @@ som_status som_destroy(som_map *m) {
     (void)hipFree(m->block_dots);
     (void)hipFree(m->xpad);
     (void)hipFree(m->sv);
-    (void)hipFree(m->sidx);
+    (void)hipFree(m->soff);
     (void)hipFree(m->sval);
-    (void)hipFree(m->spv);
-    (void)hipFree(m->sxs);
+    (void)hipFree(m->spv1);
+    (void)hipFree(m->spv2);
+    (void)hipFree(m->sst);
     (void)hipFree(m->wnorm);
     (void)hipFree(m->cand);
     (void)hipFree(m->idx1);
@@ -648,15 +649,21 @@ som_status som_train_csr(som_map *m, const int64_t *indptr, const int32_t *indic
     som::TrainArgs a = train_args(m, nullptr, n);
     a.grid = (int32_t)(ldv / 64);
     a.slot_spread = a.grid <= 64 ? 16 : 4;
+    // rows of V are addressed by 32-bit byte offsets
+    if (((uint64_t)m->d + 1) * (uint64_t)ldv * sizeof(double) > UINT32_MAX)
+        return SOM_E_UNSUPPORTED;
     const uint64_t vbytes = ((uint64_t)m->d + 3) * (uint64_t)ldv * sizeof(double);
-    const uint64_t ebytes = (uint64_t)nsteps * (uint64_t)K * 12 + (uint64_t)nsteps * 16;
+    const uint64_t ebytes = ((uint64_t)nsteps + 1) * ((uint64_t)K * 28 + sizeof(som::SparseStep));
     if (vbytes + ebytes > max_bytes()) return SOM_E_OOM;
     e = stage_steps(m, s, n, nsteps, total, a);
     if (e == hipSuccess) e = ensure(m, &m->sv, &m->sv_cap, ((int64_t)m->d + 3) * ldv);
-    if (e == hipSuccess) e = ensure(m, &m->sidx, &m->sidx_cap, nsteps * K);
-    if (e == hipSuccess) e = ensure(m, &m->sval, &m->sval_cap, nsteps * K);
-    if (e == hipSuccess) e = ensure(m, &m->spv, &m->spv_cap, nsteps * K);
-    if (e == hipSuccess) e = ensure(m, &m->sxs, &m->sxs_cap, nsteps);
+    // the call's steps and one padding step
+    const int64_t nent = (nsteps + 1) * K;
+    if (e == hipSuccess) e = ensure(m, &m->soff, &m->soff_cap, nent);
+    if (e == hipSuccess) e = ensure(m, &m->sval, &m->sval_cap, nent);
+    if (e == hipSuccess) e = ensure(m, &m->spv1, &m->spv1_cap, nent);
+    if (e == hipSuccess) e = ensure(m, &m->spv2, &m->spv2_cap, nent);
+    if (e == hipSuccess) e = ensure(m, &m->sst, &m->sst_cap, nsteps + 1);
     if (e != hipSuccess) return from_hip(e);
 
     som::SparseArgs sp{};
@@ -665,10 +672,11 @@ som_status som_train_csr(som_map *m, const int64_t *indptr, const int32_t *indic
     sp.S = m->sv + ((int64_t)m->d + 1) * ldv;
     sp.WW = sp.S + ldv;
     sp.K = K;
-    sp.sidx = m->sidx;
+    sp.soff = m->soff;
     sp.sval = m->sval;
-    sp.spv = m->spv;
-    sp.sxs = m->sxs;
+    sp.spv1 = m->spv1;
+    sp.spv2 = m->spv2;
+    sp.sst = m->sst;
     e = som::launch_prepare_train(a, m->sched, m->stream);
     if (e == hipSuccess) e = som::launch_sparse_steps(a, sp, indptr, indices, values, m->stream);
     if (e == hipSuccess) e = som::launch_sparse_enter(a, sp, m->stream);

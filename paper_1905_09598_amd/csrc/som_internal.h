@@ -140,16 +140,25 @@ hipError_t launch_qe_te_reduce(const int32_t *idx1, const int32_t *idx2,
 // of V is a scratch row that the padding entries of a step point to.
 constexpr int kSparseMaxNnz = 64;      // non-zeros per sample row
 constexpr int kSparseMaxGrid = 256;    // workgroups of 64 units
+struct SparseStep {
+    double xx;       // |x_s|^2
+    double xd1;      // x_{s-1} . x_s (0 for the call's first step)
+    double xd2;      // x_{s-2} . x_s (0 for its first two steps)
+    uint64_t both;   // bit q: entry q is a feature of x_{s-1} or x_{s-2}
+    float lr, c2;    // the step's schedule entry (lr, log2(e) / (2 sigma^2))
+};
+constexpr int kSparseStepWords = (int)(sizeof(SparseStep) / 4);
 struct SparseArgs {
     double *V;            // (d + 1) x ldv
     int64_t ldv;          // units rounded up to a multiple of 64
     double *S;            // ldv scales
     double *WW;           // ldv squared prototype norms |w_u|^2
     int32_t K;            // entries per step: 16, 32 or 64
-    int32_t *sidx;        // nsteps x K feature indices (d for padding)
-    float *sval;          // nsteps x K values (0 for padding)
-    float *spv;           // nsteps x K: the previous step's sample at sidx
-    double2 *sxs;         // nsteps x (|x_s|^2, x_{s-1} . x_s)
+    uint32_t *soff;       // nsteps x K: byte offset of the entry's row of V
+    double *sval;         // nsteps x K values (0 for padding)
+    double *spv1;         // nsteps x K: x_{s-1} at the entry's feature
+    double *spv2;         // nsteps x K: x_{s-2} at the entry's feature
+    SparseStep *sst;      // nsteps
 };
 // Per CSR row: lengths, sorted unique indices in [0, d); raises csr_bad and
 // records the longest row in csr_max_len (both zeroed first).
