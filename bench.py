@@ -7,9 +7,10 @@ full schedule (epochs * n per-sample steps in one persistent kernel), then
 assign every sample to its BMU and compute QE and TE (batched MFMA BMU).
 Data, order and initial prototypes are resident in HBM before timing starts.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload I]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload I] [--input csr]
 
-prints one JSON line.  `value` is prototype*dim updates per second of the
+prints one JSON line.  --input csr trains from the CSR form of the same rows
+(som_train_csr, the sparse-input path) and reports that kernel's own bytes.  `value` is prototype*dim updates per second of the
 whole step, T * N * d / step time.  `roofline` reports the training call:
 algorithmic bytes 3 * N * d * 4 per sample (read the prototypes for the
 distance, read and write them for the update) divided by the average
@@ -152,6 +153,9 @@ def main():
     ap.add_argument("--map-sweep", action="store_true",
                     help="instead of the bench line: per-step time of training maps of "
                          "16x16 ... 512x512 units at d = 64 (one JSON line per map size)")
+    ap.add_argument("--input", choices=("dense", "csr"), default="dense",
+                    help="train from the dense rows (som_train) or from their CSR form "
+                         "(som_train_csr, the sparse-input path)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (the "
                          "reference dispatch for scaling HBM byte counters) and exit")
@@ -190,12 +194,28 @@ def main():
     W0 = m.weights.clone()
     plan = m.plan()
     stream = torch.cuda.current_stream()
+    sparse = args.input == "csr"
+    if sparse:
+        # CSR form of the same rows (host-side input preparation, untimed)
+        nz = X != 0
+        indptr = np.zeros(cfg.n + 1, np.int64)
+        np.cumsum(nz.sum(1), out=indptr[1:])
+        r, c = np.nonzero(nz)
+        csr = (torch.from_numpy(indptr).cuda(), torch.from_numpy(c.astype(np.int32)).cuda(),
+               torch.from_numpy(X[r, c]).cuda())
+        nnz_row = np.diff(indptr)
+        # per step: the sample's non-zeros, gathered and scattered in fp64 for
+        # every unit of the 64-unit workgroups
+        sparse_bytes = float(nnz_row[order].sum()) * 2 * 8 * (-(-cfg.units // 64) * 64)
 
     def one_step(ev=None):
         m.weights = W0
         if ev is not None:
             ev[0].record(stream)
-        m.train(Xd, cfg.epochs, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1, order=od)
+        if sparse:
+            m.train_csr(*csr, cfg.epochs, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1, order=od)
+        else:
+            m.train(Xd, cfg.epochs, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1, order=od)
         if ev is not None:
             ev[1].record(stream)
         idx = m.bmu(Xd)
@@ -234,6 +254,19 @@ def main():
     alg_bytes = cfg.steps * 3.0 * cfg.units * cfg.d * 4
     achieved = alg_bytes / avg_train_s / 1e9
     traffic = measured_traffic(cfg.name)
+    kernel_name = ["train_kernel (stream)", "train_kernel (lds)",
+                   "train_pipe_kernel (stream)", "train_pipe_kernel (lds)"][plan["variant"]]
+    variant = ["stream", "lds", "pipelined-stream", "pipelined-lds"][plan["variant"]]
+    grid, block = plan["grid"], plan["block"]
+    if sparse:
+        # the sparse path's own bytes: the dense 3 N d 4 per step does not
+        # describe a kernel that touches only the sample's features
+        alg_bytes = sparse_bytes
+        achieved = alg_bytes / avg_train_s / 1e9
+        traffic = None
+        kernel_name = "sparse_train_kernel"
+        variant = "csr lazy-scale"
+        grid, block = -(-cfg.units // 64), 128
 
     out = {
         "metric": "SOM train prototype*dim updates/sec + % of HBM/MALL roofline, 1 MI355X",
@@ -253,8 +286,7 @@ def main():
             "map": f"{cfg.rows}x{cfg.cols}", "epochs": cfg.epochs,
             "train_steps_per_pass": cfg.steps,
             "schedule": f"lr {cfg.lr0}->{cfg.lr1} linear, sigma {cfg.sigma0}->{cfg.sigma1} exp",
-            "grid": plan["grid"], "block": plan["block"],
-            "variant": ["stream", "lds", "pipelined-stream", "pipelined-lds"][plan["variant"]],
+            "grid": grid, "block": block, "variant": variant, "input": args.input,
         },
         "roofline": {
             "bound": "hbm",
@@ -263,8 +295,7 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
-            "kernel": ["train_kernel (stream)", "train_kernel (lds)",
-                       "train_pipe_kernel (stream)", "train_pipe_kernel (lds)"][plan["variant"]],
+            "kernel": kernel_name,
             "kernel_ms": avg_train_s * 1e3,
             "alg_bytes_per_launch": alg_bytes,
         },
@@ -280,6 +311,10 @@ def main():
         "qe": qe,
         "te": te,
     }
+    if sparse:
+        out["roofline"]["note"] = ("sparse path: bytes = the samples' non-zeros gathered and "
+                                   "scattered in fp64 for every unit; its step is bound by the "
+                                   "grid exchange's latency, not by bytes")
     if args.cpu_budget > 0:
         out["cpu_baseline"] = cpu_baseline(cfg, X, order, args.cpu_budget)
     print(json.dumps(out), flush=True)

@@ -149,19 +149,20 @@ som_status som_train(som_map *map, const float *X, int64_t n, int32_t epochs,
  * indices and values may be NULL when indptr[n] = 0.  The schedule fields
  * mean what they mean for som_train.
  * Internally each prototype is held as a scale times an fp64 vector stored
- * feature by feature ((d + 3) * roundup(rows * cols, 64) doubles, plus
- * 12 * K + 16 bytes per step for the padded entries, K = 16, 32 or 64 from
- * the longest row; both kept by the map for later calls), so a step reads
- * and writes only the sample's features; distances are evaluated in fp64
- * and rounded once to fp32 for the BMU comparison.  The call synchronizes
- * the stream twice to validate the CSR structure before training, which is
- * then stream-ordered.
+ * feature by feature ((d + 3) * roundup(rows * cols, 64) doubles, at most
+ * 2^31 - 1 bytes for the vectors, plus 28 K + 40 bytes per step for the
+ * padded entries, K = 16, 32 or 64 from the longest row; all kept by the
+ * map for later calls), so a step reads and writes only the sample's
+ * features; distances are evaluated in fp64 and rounded once to fp32 for
+ * the BMU comparison.  The call synchronizes the stream twice to validate
+ * the CSR structure before training, which is then stream-ordered.
  * Errors: as som_train, and SOM_E_ARG (indptr NULL or not covering n + 1
  * entries, indptr[0] != 0, a row with decreasing offsets or offsets past
  * indptr[n], indices not strictly increasing within a row or outside
  * [0, d), indices or values not covering indptr[n] entries),
- * SOM_E_UNSUPPORTED (a row with more than 64 non-zeros, or more than 16,384
- * units), SOM_E_OOM (the buffers above beyond the map's memory cap). */
+ * SOM_E_UNSUPPORTED (a row with more than 64 non-zeros, more than 16,384
+ * units, or (d + 1) * roundup(rows * cols, 64) * 8 above 2^31 - 1 bytes),
+ * SOM_E_OOM (the buffers above beyond the map's memory cap). */
 som_status som_train_csr(som_map *map, const int64_t *indptr, const int32_t *indices,
                          const float *values, int64_t n, int32_t epochs,
                          const som_schedule *sched);

@@ -649,8 +649,8 @@ som_status som_train_csr(som_map *m, const int64_t *indptr, const int32_t *indic
     som::TrainArgs a = train_args(m, nullptr, n);
     a.grid = (int32_t)(ldv / 64);
     a.slot_spread = a.grid <= 64 ? 16 : 4;
-    // rows of V are addressed by 32-bit byte offsets
-    if (((uint64_t)m->d + 1) * (uint64_t)ldv * sizeof(double) > UINT32_MAX)
+    // rows of V are addressed through one buffer resource of 2^31 - 1 bytes
+    if (((uint64_t)m->d + 1) * (uint64_t)ldv * sizeof(double) > INT32_MAX)
         return SOM_E_UNSUPPORTED;
     const uint64_t vbytes = ((uint64_t)m->d + 3) * (uint64_t)ldv * sizeof(double);
     const uint64_t ebytes = ((uint64_t)nsteps + 1) * ((uint64_t)K * 28 + sizeof(som::SparseStep));
