@@ -250,3 +250,48 @@ def linear_init(mu: np.ndarray, lam, V: np.ndarray, rows: int, cols: int) -> np.
             a = 2.0 * c / (cols - 1) - 1.0 if cols > 1 else 0.0
             W[r * cols + c] = mu + a * s1 * V[:, 0] + b * s2 * V[:, 1]
     return W
+
+
+# ------------------------------------------------------------------ batch map
+# Sec. 4 names the batch form of the SOM as the variant most GPU SOMs
+# implement ([25], [26]); the paper itself trains online (Eq. (1)).  The
+# batch rule here is Kohonen's: every epoch assigns all samples to their
+# BMUs under the current prototypes, then sets each prototype to the
+# neighbourhood-weighted mean of the samples,
+#     w_u = sum_i h(u, c_i) x_i / sum_i h(u, c_i),
+# with h the Gaussian of Eq. (1) without the learning rate (a delta at the
+# BMU for sigma = 0, 1 everywhere for sigma = inf); a unit whose weights all
+# vanish keeps its prototype.  sigma decays over the epochs by the same law
+# as the online schedule, at p = e / (E - 1).  Plain numpy in fp64 on the
+# explicit N x N neighbourhood matrix.
+
+def batch_sigma(e: int, epochs: int, sigma0: float, sigma1: float,
+                sigma_decay: int = EXPONENTIAL) -> float:
+    """The radius of epoch e of a batch run of `epochs` epochs."""
+    s = schedule(1.0, 1.0, sigma0, sigma1, LINEAR, sigma_decay)
+    return schedule_at(e, epochs, s)[1]
+
+
+def train_batch(W: np.ndarray, rows: int, cols: int, X: np.ndarray, epochs: int,
+                sigma0: float, sigma1: float, sigma_decay: int = EXPONENTIAL,
+                topology: int = RECT, nthreads: Optional[int] = None, trace: bool = False):
+    """`epochs` batch epochs from W (float64 copy); returns (W, BMUs per epoch)."""
+    W = np.array(W, dtype=np.float64, order="C", copy=True)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    N = rows * cols
+    bmus = []
+    for e in range(epochs):
+        sigma = batch_sigma(e, epochs, sigma0, sigma1, sigma_decay)
+        c = evaluate(W, rows, cols, X, topology=topology, nthreads=nthreads)["c1"]
+        if trace:
+            bmus.append(c)
+        H = np.stack([neighbourhood(rows, cols, topology, k, 1.0, sigma)
+                      for k in range(N)], axis=1)          # H[u, k] = h(u, k)
+        S = np.zeros((N, X.shape[1]), dtype=np.float64)
+        np.add.at(S, c, X.astype(np.float64))
+        cnt = np.bincount(c, minlength=N).astype(np.float64)
+        num = H @ S
+        den = H @ cnt
+        keep = den > 0
+        W[keep] = num[keep] / den[keep, None]
+    return W, bmus

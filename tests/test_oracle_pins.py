@@ -384,3 +384,45 @@ def test_linear_init_spans_one_standard_deviation_per_component():
     W1 = oracle.linear_init(m, lam, V, 1, 3)
     assert np.allclose(W1[1], mu, atol=1e-12)                          # single row, centre
     assert np.allclose(W1[0], mu - 3.0 * e1, atol=1e-12)
+
+
+# ------------------------------------------------------------------ batch map
+def test_batch_radius_zero_is_a_k_means_step():
+    # sigma = 0: each prototype becomes the mean of the samples whose BMU it
+    # is; a unit without samples keeps its prototype (worked by hand)
+    X = np.array([[0, 0], [0, 1], [4, 4], [5, 5], [10, 0]], np.float32)
+    W = np.array([[0, 0.2], [4.5, 4.4], [9, 1], [20, 20]], np.float64)
+    W1, b = oracle.train_batch(W, 2, 2, X, 1, 0.0, 0.0, trace=True)
+    assert list(b[0]) == [0, 0, 1, 1, 2]
+    assert np.array_equal(W1, [[0, 0.5], [4.5, 4.5], [10, 0], [20, 20]])
+
+
+def test_batch_infinite_radius_gives_every_unit_the_global_mean():
+    X = gaussian_mixture(40, 6, 3, 0.3, seed=8)
+    W = oracle.init_uniform(2, 12, 6)
+    W1, _ = oracle.train_batch(W, 3, 4, X, 1, math.inf, math.inf)
+    mean = X.astype(np.float64).mean(0)
+    assert np.allclose(W1, np.broadcast_to(mean, W1.shape), rtol=0, atol=1e-12)
+
+
+def test_batch_two_unit_map_by_hand():
+    # samples a (3 copies) and b (2 copies) on a 1 x 2 map, a -> unit 0 and
+    # b -> unit 1; with h = exp(-1 / (2 sigma^2)) for the lattice neighbour,
+    # w0 = (3a + 2hb) / (3 + 2h) and w1 = (3ha + 2b) / (3h + 2)
+    a, b = np.array([1.0, 2.0]), np.array([5.0, -1.0])
+    X = np.array([a, a, a, b, b], np.float32)
+    W = np.array([[1.5, 2.0], [4.0, -1.0]])
+    sigma = 0.8
+    h = math.exp(-1.0 / (2 * sigma * sigma))
+    W1, _ = oracle.train_batch(W, 1, 2, X, 1, sigma, sigma)
+    assert np.allclose(W1[0], (3 * a + 2 * h * b) / (3 + 2 * h), rtol=1e-14)
+    assert np.allclose(W1[1], (3 * h * a + 2 * b) / (3 * h + 2), rtol=1e-14)
+
+
+def test_batch_radius_schedule_hits_its_endpoints():
+    assert oracle.batch_sigma(0, 5, 4.0, 0.5) == 4.0
+    assert oracle.batch_sigma(4, 5, 4.0, 0.5) == 0.5
+    assert oracle.batch_sigma(0, 1, 4.0, 0.5) == 4.0
+    mid = oracle.batch_sigma(2, 5, 4.0, 0.5, oracle.EXPONENTIAL)
+    assert mid == pytest.approx(math.sqrt(4.0 * 0.5), rel=1e-15)
+    assert oracle.batch_sigma(2, 5, 4.0, 0.5, oracle.LINEAR) == pytest.approx(2.25, rel=1e-15)
