@@ -167,6 +167,27 @@ som_status som_train_csr(som_map *map, const int64_t *indptr, const int32_t *ind
                          const float *values, int64_t n, int32_t epochs,
                          const som_schedule *sched);
 
+/* Batch-map training, the batch form of the SOM that Sec. 4 attributes to
+ * earlier GPU SOMs ([25], [26]), beside the paper's online rule (Sec. 5A):
+ * each of `epochs` epochs assigns all n rows of the device matrix X to
+ * their BMUs (as som_bmu) and then sets every prototype to the
+ * neighbourhood-weighted mean of the samples,
+ *     w_u = sum_i h(u, c_i) x_i / sum_i h(u, c_i),
+ * h(u, c) = exp(-|pos(u) - pos(c)|^2 / (2 sigma^2)) (a delta at the BMU for
+ * sigma = 0, 1 everywhere for sigma = +inf); a unit whose weights all
+ * vanish keeps its prototype.  sigma goes from sigma0 (first epoch) to
+ * sigma1 (last epoch) by sigma_decay at p = e / (epochs - 1).  Everything
+ * after the BMU is fp64: per-unit sample sums, then the lattice Gaussian as
+ * a blur along the lattice columns and then along the rows (it factors over
+ * the two axes).  Work memory of (2 + P) N (d + 1) + rows^2 + P cols^2
+ * doubles (P = 1 for RECT, 3 for HEX) is kept by the map.  Stream-ordered.
+ * Errors: SOM_E_ARG (map or X NULL, n <= 0 or above 2^31 - 1, epochs <= 0,
+ * sigma < 0 or NaN, a bad decay kind, an exponential decay with a zero or
+ * infinite endpoint, X not covering n * d floats), SOM_E_UNSUPPORTED (d
+ * above 4,194,239), SOM_E_OOM, SOM_E_DEVICE. */
+som_status som_train_batch(som_map *map, const float *X, int64_t n, int32_t epochs,
+                           double sigma0, double sigma1, int32_t sigma_decay);
+
 /* Batched BMU assignment (Sec. 8A): for each of the n rows of the device
  * matrix X, out_idx[i] = BMU index (lowest index among equal minima).
  * Candidates are ranked with fp32 matrix-core products

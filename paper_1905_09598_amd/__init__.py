@@ -24,8 +24,8 @@ from typing import Optional
 __all__ = [
     "SomError", "LibraryMissing", "Schedule", "Map", "lib", "library_path",
     "som_create", "som_destroy", "som_set_topology", "som_set_stream",
-    "som_train", "som_train_csr", "som_bmu", "som_bmu2", "som_quantization_error",
-    "som_topographic_error", "som_get_weights", "som_set_weights",
+    "som_train", "som_train_csr", "som_train_batch", "som_bmu", "som_bmu2",
+    "som_quantization_error", "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
     "som_pca2", "som_suggest_size", "som_init_linear",
     "som_status_string", "RECT", "HEX", "LINEAR", "EXPONENTIAL", "EXPORTED",
@@ -44,7 +44,7 @@ STATUS = {0: "SOM_OK", 1: "SOM_E_ARG", 2: "SOM_E_OOM", 3: "SOM_E_DEVICE",
 # Every symbol include/som.h declares.
 EXPORTED = (
     "som_create", "som_destroy", "som_set_topology", "som_set_stream",
-    "som_train", "som_train_csr", "som_bmu", "som_bmu2", "som_quantization_error",
+    "som_train", "som_train_csr", "som_train_batch", "som_bmu", "som_bmu2", "som_quantization_error",
     "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
     "som_pca2", "som_suggest_size", "som_init_linear", "som_status_string",
@@ -97,6 +97,7 @@ def lib():
         "som_set_stream": [vp, vp],
         "som_train": [vp, vp, i64, i32, C.POINTER(Schedule)],
         "som_train_csr": [vp, vp, vp, vp, i64, i32, C.POINTER(Schedule)],
+        "som_train_batch": [vp, vp, i64, i32, C.c_double, C.c_double, i32],
         "som_bmu": [vp, vp, i64, vp],
         "som_bmu2": [vp, vp, i64, vp, vp, vp],
         "som_quantization_error": [vp, vp, i64, C.POINTER(C.c_double)],
@@ -189,6 +190,12 @@ def som_train_csr(handle: int, indptr, indices, values, n: int, epochs: int,
                   sched: Schedule) -> None:
     _check(lib().som_train_csr(handle, _ptr(indptr), _ptr(indices), _ptr(values), n, epochs,
                                C.byref(sched)), "som_train_csr")
+
+
+def som_train_batch(handle: int, X, n: int, epochs: int, sigma0: float, sigma1: float,
+                    sigma_decay: int = EXPONENTIAL) -> None:
+    _check(lib().som_train_batch(handle, _ptr(X), n, epochs, float(sigma0), float(sigma1),
+                                 int(sigma_decay)), "som_train_batch")
 
 
 def som_bmu(handle: int, X, n: int, out_idx) -> None:
@@ -362,6 +369,15 @@ class Map:
         nnz = indices.numel()
         som_train_csr(self.handle, indptr, indices if nnz else None, values if nnz else None,
                       indptr.numel() - 1, int(epochs), s)
+
+    def train_batch(self, X, epochs: int, sigma0: float, sigma1: float,
+                    sigma_decay: int = EXPONENTIAL) -> None:
+        """Batch-map epochs over the rows of X (see som_train_batch)."""
+        _require(X, "float32", "X")
+        if X.dim() != 2 or X.shape[1] != self.d:
+            raise ValueError(f"X must be (n, {self.d})")
+        self._bind_stream()
+        som_train_batch(self.handle, X, X.shape[0], int(epochs), sigma0, sigma1, sigma_decay)
 
     def bmu(self, X, second: bool = False):
         _require(X, "float32", "X")

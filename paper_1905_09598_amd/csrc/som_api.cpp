@@ -52,6 +52,9 @@ struct som_map {
     double *sval = nullptr, *spv1 = nullptr, *spv2 = nullptr;
     som::SparseStep *sst = nullptr;
     int64_t soff_cap = 0, sval_cap = 0, spv1_cap = 0, spv2_cap = 0, sst_cap = 0;
+    // batch-map work memory (som_batch.hip)
+    double *bwork = nullptr;
+    int64_t bwork_cap = 0;
     // evaluation scratch
     float *wnorm = nullptr;
     int32_t *cand = nullptr, *idx1 = nullptr, *idx2 = nullptr;
@@ -308,6 +311,7 @@ som_status som_destroy(som_map *m) {
     (void)hipFree(m->sched);
     (void)hipFree(m->block_dots);
     (void)hipFree(m->xpad);
+    (void)hipFree(m->bwork);
     (void)hipFree(m->sv);
     (void)hipFree(m->soff);
     (void)hipFree(m->sval);
@@ -683,6 +687,56 @@ som_status som_train_csr(som_map *m, const int64_t *indptr, const int32_t *indic
     if (e == hipSuccess) e = som::launch_train_sparse(a, sp, m->stream);
     if (e == hipSuccess) e = som::launch_sparse_leave(a, sp, m->stream);
     return from_hip(e);
+}
+
+som_status som_train_batch(som_map *m, const float *X, int64_t n, int32_t epochs,
+                           double sigma0, double sigma1, int32_t sigma_decay) {
+    if (!m || !X || n <= 0 || n > INT32_MAX || epochs <= 0) return SOM_E_ARG;
+    som_schedule s{};
+    s.lr0 = s.lr1 = 1.0;
+    s.lr_decay = SOM_DECAY_LINEAR;
+    s.sigma0 = sigma0;
+    s.sigma1 = sigma1;
+    s.sigma_decay = sigma_decay;
+    if (!schedule_ok(&s)) return SOM_E_ARG;
+    if (!device_range_ok(X, (uint64_t)n * (uint64_t)m->d * sizeof(float))) return SOM_E_ARG;
+    const size_t work = som::batch_work_doubles(m->rows, m->cols, m->d, m->topology);
+    if (((uint64_t)m->d + 1 + 63) / 64 > 65535) return SOM_E_UNSUPPORTED;
+    if ((uint64_t)work * sizeof(double) > max_bytes()) return SOM_E_OOM;
+    hipError_t e = ensure(m, &m->bwork, &m->bwork_cap, (int64_t)work);
+    if (e != hipSuccess) return from_hip(e);
+    som_status st = ensure_eval_scratch(m, n, 0);
+    if (st != SOM_OK) return st;
+    for (int32_t ep = 0; ep < epochs; ++ep) {
+        // the radius at p = ep / (epochs - 1), endpoints exact
+        const double p = epochs > 1 ? (double)ep / (double)(epochs - 1) : 0.0;
+        double sigma = sigma0;
+        if (sigma0 != sigma1) {
+            if (p == 1.0)
+                sigma = sigma1;
+            else if (p != 0.0)
+                sigma = sigma_decay == SOM_DECAY_LINEAR
+                            ? (1.0 - p) * sigma0 + p * sigma1
+                            : pow(sigma0, 1.0 - p) * pow(sigma1, p);
+        }
+        st = run_eval(m, X, n, m->idx1, nullptr, nullptr);
+        if (st != SOM_OK) return st;
+        som::BatchArgs b{};
+        b.bmu = m->idx1;
+        b.X = X;
+        b.n = n;
+        b.d = m->d;
+        b.rows = m->rows;
+        b.cols = m->cols;
+        b.topology = m->topology;
+        b.sigma = sigma;
+        b.work = m->bwork;
+        b.W = m->W;
+        b.ld = m->ld;
+        e = som::launch_batch_epoch(b, m->stream);
+        if (e != hipSuccess) return from_hip(e);
+    }
+    return SOM_OK;
 }
 
 som_status som_bmu2(som_map *m, const float *X, int64_t n, int32_t *out_idx,

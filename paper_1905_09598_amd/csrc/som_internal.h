@@ -172,6 +172,20 @@ hipError_t launch_sparse_enter(const TrainArgs &a, const SparseArgs &sp, hipStre
 hipError_t launch_sparse_leave(const TrainArgs &a, const SparseArgs &sp, hipStream_t s);
 hipError_t launch_train_sparse(const TrainArgs &a, const SparseArgs &sp, hipStream_t s);
 
+// Batch-map training (som_batch.hip): one epoch after the BMUs are known.
+struct BatchArgs {
+    const int32_t *bmu;     // n BMU indices
+    const float *X;         // n x d, row-major
+    int64_t n;
+    int32_t d, rows, cols, topology;
+    double sigma;           // the epoch's radius
+    double *work;           // batch_work_doubles(rows, cols, d, topology)
+    float *W;               // N x ld prototypes, updated in place
+    int64_t ld;
+};
+size_t batch_work_doubles(int32_t rows, int32_t cols, int32_t d, int32_t topology);
+hipError_t launch_batch_epoch(const BatchArgs &b, hipStream_t s);
+
 // Principal components and linear initialisation (som_pca.hip).
 constexpr int kPcaBlock = 8;  // subspace-iteration block
 // Floats of work memory for pca_top2 (covariance d x d, iteration vectors,

@@ -52,6 +52,7 @@ def test_calls_on_null_map_are_argument_errors():
     s = som.make_schedule(0.5, 0.01, 3.0, 1.0)
     assert L.som_train(None, None, 10, 1, C.byref(s)) == 1
     assert L.som_train_csr(None, None, None, None, 10, 1, C.byref(s)) == 1
+    assert L.som_train_batch(None, None, 10, 1, 2.0, 1.0, 1) == 1
     assert L.som_bmu(None, None, 10, None) == 1
     assert L.som_bmu2(None, None, 10, None, None, None) == 1
     assert L.som_synchronize(None) == 1
