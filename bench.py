@@ -141,6 +141,40 @@ def map_sweep(cpu_budget: float):
         m.close()
 
 
+def batch_map_epoch(workload: int, steps: int, warmup: int):
+    """Milliseconds per batch-map epoch (som_train_batch at the workload's
+    starting radius), HIP events on the map's stream."""
+    import torch
+
+    import paper_1905_09598_amd as som
+    import workloads
+
+    cfg = workloads.WORKLOADS[workload]
+    Xd = torch.from_numpy(workloads.make_data(cfg)).cuda()
+    m = som.Map(cfg.rows, cfg.cols, cfg.d, seed=cfg.init_seed)
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        m.train_batch(Xd, 1, cfg.sigma0, cfg.sigma0)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for a, b in ev:
+        a.record(stream)
+        m.train_batch(Xd, 1, cfg.sigma0, cfg.sigma0)
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in ev)[len(ev) // 2]
+    bmu_flops = 2.0 * cfg.n * cfg.units * cfg.d
+    print(json.dumps({
+        "metric": "batch-map epoch time (BMU of every sample, fp64 neighbourhood means)",
+        "value": ms, "unit": "ms per epoch", "higher_is_better": False, "steps": steps,
+        "data": "synthetic", "config": {"workload": cfg.name, "n": cfg.n, "d": cfg.d,
+                                        "map": f"{cfg.rows}x{cfg.cols}", "sigma": cfg.sigma0},
+        "bmu_flops_per_epoch": bmu_flops,
+        "epoch_tflops_bmu_equivalent": bmu_flops / (ms / 1e3) / 1e12,
+    }), flush=True)
+    m.close()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -153,6 +187,9 @@ def main():
     ap.add_argument("--map-sweep", action="store_true",
                     help="instead of the bench line: per-step time of training maps of "
                          "16x16 ... 512x512 units at d = 64 (one JSON line per map size)")
+    ap.add_argument("--batch-map", action="store_true",
+                    help="instead of the bench line: time one batch-map epoch "
+                         "(som_train_batch) on the workload, one JSON line")
     ap.add_argument("--input", choices=("dense", "csr"), default="dense",
                     help="train from the dense rows (som_train) or from their CSR form "
                          "(som_train_csr, the sparse-input path)")
@@ -171,6 +208,9 @@ def main():
         return
     if args.map_sweep:
         map_sweep(args.cpu_budget)
+        return
+    if args.batch_map:
+        batch_map_epoch(args.workload, args.steps, args.warmup)
         return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not "
