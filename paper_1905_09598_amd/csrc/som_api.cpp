@@ -375,6 +375,11 @@ static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
     const char *v = getenv("SOM_TRAIN_VARIANT");
     a.variant = (v && *v) ? atoi(v) : 0;
     if (a.variant < 0 || a.variant > 5) a.variant = 0;
+    // SOM_TRAIN_LDS_ROWS: rows per workgroup the pipelined streamed variant
+    // keeps in LDS (at most what fits); unset = as many as fit.
+    const char *lr = getenv("SOM_TRAIN_LDS_ROWS");
+    a.lds_rows = (lr && *lr) ? atoi(lr) : -1;
+    if (a.lds_rows < -1) a.lds_rows = -1;
     a.timeout_ticks = 100000000ull * 20;  // 20 s at the 100 MHz reference clock
     return a;
 }

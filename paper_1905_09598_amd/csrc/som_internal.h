@@ -48,6 +48,8 @@ struct TrainArgs {
     DevState *state;
     int32_t grid;           // requested workgroups (0 = planner's choice)
     int32_t variant;        // requested variant: 0 any, 1 LDS-resident, 2 streamed
+    int32_t lds_rows;       // pipelined streamed variant: leading rows of each
+                            // workgroup kept in LDS (-1 = planner's choice)
     uint64_t timeout_ticks; // bound of one exchange wait, in 100 MHz ticks
 };
 
@@ -57,6 +59,7 @@ struct TrainPlan {
     int32_t variant = 0;     // 0 streamed, 1 LDS-resident, 2 / 3 pipelined streamed / LDS
     int32_t block_m = 0;     // steps per block of the chosen kernel instance
     int32_t kslots = 0;      // float4 columns per lane (template instance)
+    int32_t lds_rows = 0;    // pipelined streamed variant: rows per workgroup in LDS
     int32_t slot_spread = 1;
     size_t lds_bytes = 0;
 };

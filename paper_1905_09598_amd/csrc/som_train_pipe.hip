@@ -162,11 +162,13 @@ __device__ inline float dot4(f4 a, f4 b, float acc) {
 // and f.(xn_j - z) (BDOT), reduced over the wave into
 // dots[(r * 3 + sweeper) * 2M + ...] (complete in lane 63).  Rows (and their
 // coefficients) are loaded D rows ahead, into a ring of registers indexed
-// statically.
+// statically.  Callers sweeping a part of the rows pass coef_prev and dots
+// advanced to its first row.
 template <int M, int KS, int D, bool LDSW, bool MAT, bool ADOT, bool BDOT>
 __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&xp)[M][KS],
                                   const f4 (&xc)[M][KS], const f4 (&xn)[M][KS],
                                   const float *coef_prev, float *dots) {
+    if (R <= 0) return;
     constexpr int ND = 2 * M;
     constexpr bool DOTS = ADOT || BDOT;
     row_t<LDSW> *rows = rows_as<LDSW>(rows_p);
@@ -244,6 +246,21 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
     }
 }
 
+// A sweep over the workgroup's R rows: rows [0, RL) from LDS (loaded two
+// ahead) and, in the streamed variant (LDSW false), rows [RL, R) from
+// memory at gs (loaded four ahead).
+template <int M, int KS, bool LDSW, bool MAT, bool ADOT, bool BDOT>
+__device__ inline void sweep_rows(f4 *lw, int RL, f4 *gs, int R, int P4, int nw,
+                                  const f4 (&xp)[M][KS], const f4 (&xc)[M][KS],
+                                  const f4 (&xn)[M][KS], const float *coef_prev, float *dots) {
+    constexpr int ND = 2 * M;
+    pipe_sweep<M, KS, 2, true, MAT, ADOT, BDOT>(lw, RL, P4, nw, xp, xc, xn, coef_prev, dots);
+    if constexpr (!LDSW)
+        pipe_sweep<M, KS, 4, false, MAT, ADOT, BDOT>(gs, R - RL, P4, nw, xp, xc, xn,
+                                                     coef_prev + (size_t)RL * (M + 1),
+                                                     dots + (size_t)RL * kSweepers * ND);
+}
+
 // ---------------------------------------------------------------- controller
 // Controller lane r (< R): Gram matrix E of the next block from the sweep's
 // products of row r (d: f.f, f.A_1.., f.B_0.., summed over the sweepers),
@@ -302,7 +319,6 @@ template <int M, int KS, bool LDSW>
 __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
     constexpr int T = M * (M + 1) / 2;
     constexpr int ND = 2 * M;
-    constexpr int D = LDSW ? 2 : 4;  // rows loaded ahead of their use
     extern __shared__ __align__(16) unsigned char smem[];
     const int G = a.grid, b = blockIdx.x, tid = threadIdx.x;
     const int wave = tid >> 6, lane = tid & 63;
@@ -324,13 +340,15 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
     }
     if (tid == 0) bc->abort = 0;
     f4 *gw = reinterpret_cast<f4 *>(a.W) + (int64_t)r0 * P4;
-    f4 *rows = gw;
-    if (LDSW) {
+    // Rows [0, RL) live in LDS for the whole launch; the streamed variant
+    // keeps as many as its LDS holds (planner) and streams the rest.
+    const int RL = LDSW ? R : (a.lds_rows < R ? (a.lds_rows > 0 ? a.lds_rows : 0) : R);
+    if (RL > 0) {
         row_t<true> *lw = rows_as<true>(l.lw);
         const row_t<false> *g = rows_as<false>(gw);
-        for (int e = tid; e < R * P4; e += 256) lw[e] = g[e];
-        rows = l.lw;
+        for (int e = tid; e < RL * P4; e += 256) lw[e] = g[e];
     }
+    f4 *gs = gw + (int64_t)RL * P4;  // first streamed row
     const int64_t nb = (a.nsteps + M - 1) / M;
     __syncthreads();
     // The controller and the sweepers run separate loops over the blocks that
@@ -394,8 +412,8 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
         if (nb > 1) load_samples<M, KS>(xn, a, 1, own);
         // Products of the initial prototypes with block 0 (centred on its
         // first sample): f.f and f.(x_{0,i} - z), parity 1.
-        pipe_sweep<M, KS, D, LDSW, false, true, false>(rows, R, P4, nw, xc, xc, xc, l.coef,
-                                                       l.dots + (size_t)l.Rp * kSweepers * ND);
+        sweep_rows<M, KS, LDSW, false, true, false>(l.lw, RL, gs, R, P4, nw, xc, xc, xc, l.coef,
+                                                 l.dots + (size_t)l.Rp * kSweepers * ND);
         __syncthreads();
         for (int64_t blk = 0; blk < nb; ++blk) {
             const int par = (int)(blk & 1);
@@ -404,11 +422,11 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
             const bool has_next = blk + 1 < nb;
             if (blk == 0) {
                 if (has_next)
-                    pipe_sweep<M, KS, D, LDSW, false, true, true>(rows, R, P4, nw, xp, xc, xn, cp, dd);
+                    sweep_rows<M, KS, LDSW, false, true, true>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp, dd);
             } else if (has_next) {
-                pipe_sweep<M, KS, D, LDSW, true, true, true>(rows, R, P4, nw, xp, xc, xn, cp, dd);
+                sweep_rows<M, KS, LDSW, true, true, true>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp, dd);
             } else {
-                pipe_sweep<M, KS, D, LDSW, true, false, false>(rows, R, P4, nw, xp, xc, xn, cp, dd);
+                sweep_rows<M, KS, LDSW, true, false, false>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp, dd);
             }
 #pragma unroll
             for (int j = 0; j < M; ++j)
@@ -422,14 +440,15 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
             if (bc->abort) return;
         }
         // apply the last block's updates
-        pipe_sweep<M, KS, D, LDSW, true, false, false>(
-            rows, R, P4, nw, xp, xc, xn, l.coef + (size_t)((nb - 1) & 1) * l.Rp * (M + 1), l.dots);
+        sweep_rows<M, KS, LDSW, true, false, false>(
+            l.lw, RL, gs, R, P4, nw, xp, xc, xn, l.coef + (size_t)((nb - 1) & 1) * l.Rp * (M + 1),
+            l.dots);
     }
-    if (LDSW) {
+    if (RL > 0) {
         __syncthreads();
         const row_t<true> *lw = rows_as<true>(l.lw);
         row_t<false> *g = rows_as<false>(gw);
-        for (int e = tid; e < R * P4; e += 256) g[e] = lw[e];
+        for (int e = tid; e < RL * P4; e += 256) g[e] = lw[e];
     }
 }
 
@@ -484,13 +503,22 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
     for (const PipeInstance &pi : kPipe) {
         if (pi.ks != ks_need) continue;
         for (int v = 0; v < 2; ++v) {
-            const bool ldsw = v == 1;
+            const bool ldsw = v == 0;  // LDS first: it wins ties
             if ((a.variant == 1 && !ldsw) || (a.variant == 2 && ldsw)) continue;
             if (!ldsw && !pi.stream_ok) continue;
             for (int g = 1;; g = (g * 2 > max_grid && g < max_grid) ? max_grid : g * 2) {
                 const int gg = a.grid > 0 ? (a.grid < a.N ? a.grid : a.N) : g;
                 const int rmax = (a.N + gg - 1) / gg;
-                if (rmax <= 64 && pipe_lds_bytes(pi.m, rmax, P4, ldsw) <= (size_t)max_lds) {
+                // The streamed variant keeps as many leading rows as its LDS
+                // holds (or a.lds_rows when set) and streams the rest.
+                const size_t base = pipe_lds_bytes(pi.m, rmax, P4, ldsw);
+                int rl = ldsw ? rmax : 0;
+                if (!ldsw && base < (size_t)max_lds) {
+                    const int64_t fit = ((int64_t)max_lds - (int64_t)base) / (P4 * 16);
+                    rl = (int)(fit < rmax ? fit : rmax);
+                    if (a.lds_rows >= 0) rl = a.lds_rows < rl ? a.lds_rows : rl;
+                }
+                if (rmax <= 64 && base <= (size_t)max_lds) {
                     // Calibrated on MI355X.  Controller: about one exchange
                     // plus 0.1 us per step and 1.2 us per block.  Sweeper:
                     // a row slice costs ~(20 M + 4) VALU instructions and a
@@ -500,10 +528,9 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                     // at least the read and write of the workgroup's rows at
                     // its share of 8 TB/s.
                     const double item_us = (20.0 * pi.m + 4) * 4.0 / 2400.0;
-                    const double row_us = ks_need * item_us + (88.0 * pi.m + 400) / 2400.0 +
-                                          (ldsw ? 0.0 : 0.3);
-                    const double visit_us = rmax * row_us;
-                    const double mem_us = ldsw ? 0.0 : rmax * P4 * 32.0 / (8e6 / gg);
+                    const double row_us = ks_need * item_us + (88.0 * pi.m + 400) / 2400.0;
+                    const double visit_us = rmax * row_us + (rmax - rl) * 0.3;
+                    const double mem_us = (rmax - rl) * P4 * 32.0 / (8e6 / gg);
                     const double sweep = (visit_us > mem_us ? visit_us : mem_us) / pi.m;
                     const double ctl = exchange_us(gg) + 0.1;
                     const double t = (sweep > ctl ? sweep : ctl) + 1.2 / pi.m;
@@ -513,6 +540,7 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                         plan->variant = ldsw ? 3 : 2;
                         plan->block_m = pi.m;
                         plan->kslots = pi.ks;
+                        plan->lds_rows = ldsw ? 0 : rl;
                     }
                 }
                 if (a.grid > 0 || g >= max_grid) break;
@@ -521,7 +549,8 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
     }
     if (best < 1e300) {
         plan->lds_bytes = pipe_lds_bytes(plan->block_m, (a.N + plan->grid - 1) / plan->grid, P4,
-                                          plan->variant == 3);
+                                          plan->variant == 3) +
+                          (size_t)plan->lds_rows * P4 * 16;
         if (plan->lds_bytes < 84 * 1024) plan->lds_bytes = 84 * 1024;
         plan->block = 256;
         plan->slot_spread = plan->grid <= 64 ? 16 : 4;
@@ -551,6 +580,7 @@ hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStrea
     TrainArgs args = a;
     args.grid = plan.grid;
     args.slot_spread = plan.slot_spread;
+    args.lds_rows = plan.variant == 3 ? 0 : plan.lds_rows;
     const int64_t nb = (a.nsteps + pi->m - 1) / pi->m;
     pi->dots<<<dim3((unsigned)nb), dim3(256), 0, s>>>(args, args.block_dots, nb);
     hipError_t e = hipGetLastError();

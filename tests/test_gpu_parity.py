@@ -430,6 +430,21 @@ def test_training_shapes_follow_the_oracle(rows, cols, d, n, epochs, variant, mo
         assert plan["variant"] in (0, 1)
 
 
+@pytest.mark.parametrize("lds_rows", ["0", "1", "7", "64"])
+@pytest.mark.parametrize("rows,cols,d,n,epochs", [(20, 13, 1500, 61, 2), (11, 12, 2048, 40, 1)])
+def test_streamed_variant_with_leading_rows_in_lds(rows, cols, d, n, epochs, lds_rows,
+                                                   monkeypatch):
+    # the streamed pipelined kernel keeps its first rows in LDS and streams
+    # the rest; 8 workgroups give 33 (16) rows each, so 0, 1 and 7 split the
+    # rows and 64 keeps as many as fit
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", "4")
+    monkeypatch.setenv("SOM_TRAIN_GRID", "8")
+    monkeypatch.setenv("SOM_TRAIN_LDS_ROWS", lds_rows)
+    say("streamed + LDS rows", rows, cols, d, n, epochs, "lds_rows", lds_rows)
+    plan = _train_vs_oracle(rows, cols, d, n, epochs)
+    assert plan["variant"] == 2 and plan["grid"] == 8
+
+
 def test_misaligned_samples_train_like_aligned_ones():
     # X starting one float into an allocation (d % 4 == 0 but rows not
     # 16-byte aligned) goes through the padded copy; results are bitwise

@@ -330,18 +330,20 @@ def test_malformed_csr_is_rejected():
 
 
 # --------------------------------------------------------------- end to end
-@pytest.mark.parametrize("ci", [0, 1, 2, 3])
-def test_full_training_matches_oracle_quality(ci):
+@pytest.mark.parametrize("ci,topology", [(0, som.RECT), (1, som.RECT), (2, som.RECT),
+                                         (3, som.RECT), (0, som.HEX), (1, som.HEX),
+                                         (2, som.HEX)])
+def test_full_training_matches_oracle_quality(ci, topology):
     cfg = config(ci)
-    g = golden(cfg)
+    g = golden(cfg, hex_lattice=topology == som.HEX)
     if g is None:
         pytest.skip(f"no oracle golden values for {cfg.name} yet")
-    say("sparse e2e", cfg.name)
+    say("sparse e2e", cfg.name, "hex" if topology else "rect")
     X = workloads.make_data(cfg)
     order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)
     assert workloads.sha256_of(X) == g["sha256_X"]
     assert workloads.sha256_of(order) == g["sha256_order"]
-    m = som.Map(cfg.rows, cfg.cols, cfg.d, seed=cfg.init_seed)
+    m = som.Map(cfg.rows, cfg.cols, cfg.d, seed=cfg.init_seed, topology=topology)
     m.train_csr(*csr(X), cfg.epochs, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1,
                 order=dev(order))
     Xd = dev(X)
