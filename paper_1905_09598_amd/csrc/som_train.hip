@@ -67,13 +67,16 @@ __device__ inline void load_block(f4 (&x)[M][K], const TrainArgs &a, int64_t s_b
     }
 }
 
-// One pass over the workgroup's R rows.  UPD applies the block's updates
-// from coef[r] = (beta, gamma_0..gamma_{M-1}); GRAM accumulates the Gram
-// matrix of e_j = xg_j - w over the (updated) row into E[r] (or, with more
-// than one wave per row, the wave's partials into part[(r * T + t) * WPR + w]).
+// One pass over R rows.  UPD applies the block's updates from coef[r] =
+// (beta, gamma_0..gamma_{M-1}); GRAM accumulates the Gram matrix of
+// e_j = xg_j - w over the (updated) row into E[r] (or, with more than one
+// wave per row, the wave's partials into part[(r * T + t) * WPR + w]).
+// Callers sweeping a part of the rows pass coef, E and part advanced to its
+// first row.
 template <int K, int L, int M, int U, bool LDSW, bool UPD, bool GRAM>
 __device__ inline void sweep(f4 *rows_p, int R, const f4 (&xu)[M][K], const f4 (&xg)[M][K],
                              const float *coef, float *E, float *part) {
+    if (R <= 0) return;
     row_t<LDSW> *__restrict__ rows = rows_as<LDSW>(rows_p);
     constexpr int P = kTrainBlock / L;
     constexpr int P4 = L * K;
@@ -149,6 +152,20 @@ __device__ inline void sweep(f4 *rows_p, int R, const f4 (&xu)[M][K], const f4 (
             }
         }
     }
+}
+
+// A pass over the workgroup's R rows: rows [0, RL) in LDS and, in the
+// streamed variant (LDSW false), rows [RL, R) in memory at gs.
+template <int K, int L, int M, int U, bool LDSW, bool UPD, bool GRAM>
+__device__ inline void sweep_rows(f4 *lw, int RL, f4 *gs, int R, const f4 (&xu)[M][K],
+                                  const f4 (&xg)[M][K], const float *coef, float *E,
+                                  float *part) {
+    constexpr int T = M * (M + 1) / 2;
+    constexpr int WPR = L / 64;
+    sweep<K, L, M, U, true, UPD, GRAM>(lw, RL, xu, xg, coef, E, part);
+    if constexpr (!LDSW)
+        sweep<K, L, M, U, false, UPD, GRAM>(gs, R - RL, xu, xg, coef + (size_t)RL * (M + 1),
+                                            E + (size_t)RL * T, part + (size_t)RL * T * WPR);
 }
 
 // Wave 0 only: the BMUs of the block's mb steps, s0 .. s0 + mb - 1, from the
@@ -264,7 +281,7 @@ __device__ inline Layout layout(unsigned char *smem, int R) {
 // with samples xg, then the samples of the block after next go into xu.
 template <int K, int L, int M, int U, bool LDSW>
 __device__ inline bool run_block(const TrainArgs &a, int64_t blk, int64_t nblocks, int r0,
-                                 int R, f4 *rows, const Layout &l, f4 (&xu)[M][K],
+                                 int R, int RL, f4 *gs, const Layout &l, f4 (&xu)[M][K],
                                  const f4 (&xg)[M][K], StepWindow<int> &ow,
                                  StepWindow<float2> &sw, Bcast *bc) {
     const int wave = threadIdx.x >> 6;
@@ -277,9 +294,9 @@ __device__ inline bool run_block(const TrainArgs &a, int64_t blk, int64_t nblock
     __syncthreads();
     if (bc->abort) return false;
     if (blk + 1 < nblocks)
-        sweep<K, L, M, U, LDSW, true, true>(rows, R, xu, xg, l.coef, l.E, l.part);
+        sweep_rows<K, L, M, U, LDSW, true, true>(l.lw, RL, gs, R, xu, xg, l.coef, l.E, l.part);
     else
-        sweep<K, L, M, U, LDSW, true, false>(rows, R, xu, xg, l.coef, l.E, l.part);
+        sweep_rows<K, L, M, U, LDSW, true, false>(l.lw, RL, gs, R, xu, xg, l.coef, l.E, l.part);
     if (blk + 2 < nblocks) load_block<K, L, M>(xu, a, (blk + 2) * M, ow);
     __syncthreads();
     return true;
@@ -304,11 +321,11 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
         l.pos[r] = make_float4((float)ur, (float)uc, (float)(ur & 1), 0.f);
     }
     f4 *gw = reinterpret_cast<f4 *>(a.W) + (int64_t)r0 * P4;
-    f4 *rows = gw;
-    if (LDSW) {
-        for (int e = tid; e < R * P4; e += kTrainBlock) l.lw[e] = gw[e];
-        rows = l.lw;
-    }
+    // Rows [0, RL) live in LDS for the whole launch; the streamed variant
+    // keeps as many as its LDS holds (planner) and streams the rest.
+    const int RL = LDSW ? R : (a.lds_rows < R ? (a.lds_rows > 0 ? a.lds_rows : 0) : R);
+    for (int e = tid; e < RL * P4; e += kTrainBlock) l.lw[e] = gw[e];
+    f4 *gs = gw + (int64_t)RL * P4;  // first streamed row
 
     StepWindow<int> ow;      // sample indices
     StepWindow<float2> sw;   // schedule entries (wave 0)
@@ -320,17 +337,18 @@ __global__ __launch_bounds__(kTrainBlock, 1) void train_kernel(TrainArgs a) {
     if (nblocks > 1) load_block<K, L, M>(xB, a, M, ow);
     __syncthreads();
     // Gram matrices of block 0 against the initial prototypes.
-    sweep<K, L, M, U, LDSW, false, true>(rows, R, xA, xA, l.coef, l.E, l.part);
+    sweep_rows<K, L, M, U, LDSW, false, true>(l.lw, RL, gs, R, xA, xA, l.coef, l.E, l.part);
     __syncthreads();
 
     for (int64_t blk = 0; blk < nblocks; blk += 2) {
-        if (!run_block<K, L, M, U, LDSW>(a, blk, nblocks, r0, R, rows, l, xA, xB, ow, sw, bc)) return;
+        if (!run_block<K, L, M, U, LDSW>(a, blk, nblocks, r0, R, RL, gs, l, xA, xB, ow, sw, bc))
+            return;
         if (blk + 1 < nblocks &&
-            !run_block<K, L, M, U, LDSW>(a, blk + 1, nblocks, r0, R, rows, l, xB, xA, ow, sw, bc))
+            !run_block<K, L, M, U, LDSW>(a, blk + 1, nblocks, r0, R, RL, gs, l, xB, xA, ow, sw,
+                                         bc))
             return;
     }
-    if (LDSW)
-        for (int e = tid; e < R * P4; e += kTrainBlock) gw[e] = l.lw[e];
+    for (int e = tid; e < RL * P4; e += kTrainBlock) gw[e] = l.lw[e];
 }
 
 typedef void (*TrainKernel)(TrainArgs);
@@ -389,14 +407,15 @@ double exchange_us_impl(int g) {
 }
 
 // Sweep time per step: VALU issue of the rows of one lane group (4 cycles
-// per wave64 instruction at 2.4 GHz) and, for streamed rows, memory traffic
-// at about 30 GB/s per CU; both spread over the block's M steps.
-double sweep_us(const Instance &in, int rmax, bool ldsw) {
+// per wave64 instruction at 2.4 GHz) and, for the streamed rows (all but
+// the rl kept in LDS), memory traffic at about 30 GB/s per CU; both spread
+// over the block's M steps.
+double sweep_us(const Instance &in, int rmax, bool ldsw, int rl) {
     const double P = 256.0 / in.lanes, M = in.m, T = M * (M + 1) / 2;
     const double rows = ceil(rmax / P);
     const double instr_per_row = in.k * (4 * M + 4 * T + 4 * (M + 1)) + 12 * T + 20;
     const double valu = rows * instr_per_row * 4 / 2400.0;
-    const double mem = ldsw ? 0.0 : rmax * 2.0 * 16.0 * in.lanes * in.k / 30e3;
+    const double mem = ldsw ? 0.0 : (rmax - rl) * 2.0 * 16.0 * in.lanes * in.k / 30e3;
     return (valu > mem ? valu : mem) / M + 1.0 / M;
 }
 
@@ -427,6 +446,16 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     }
     if (!in) return hipErrorInvalidValue;
 
+    // The streamed variant keeps as many leading rows per workgroup in LDS
+    // as fit beside its per-row state (or a.lds_rows when set).
+    const int64_t row_bytes = (int64_t)in->lanes * in->k * 16;
+    auto lds_rows_for = [&](int rmax) {
+        const int64_t base = (int64_t)lds_bytes_for(*in, rmax, false);
+        int64_t rl = base < max_lds ? ((int64_t)max_lds - base) / row_bytes : 0;
+        if (rl > rmax) rl = rmax;
+        if (a.lds_rows >= 0 && a.lds_rows < rl) rl = a.lds_rows;
+        return (int)rl;
+    };
     int grid = 0, variant = 0;
     if (a.grid > 0) {
         grid = a.grid < a.N ? a.grid : a.N;
@@ -435,12 +464,14 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
         if (a.variant == 1 && variant == 0) return hipErrorInvalidValue;
     } else {
         double best = 1e300;
-        for (int v = 0; v < 2; ++v) {
+        for (int v = 1; v >= 0; --v) {  // LDS first: it wins ties
             if ((v == 0 && a.variant == 1) || (v == 1 && a.variant == 2)) continue;
             for (int g = 1;; g = g * 2 > max_grid && g < max_grid ? max_grid : g * 2) {
                 const int rmax = (a.N + g - 1) / g;
                 if (v == 0 || lds_bytes_for(*in, rmax, true) <= (size_t)max_lds) {
-                    const double t = exchange_us_impl(g) + sweep_us(*in, rmax, v == 1) + 0.3;
+                    const double t = exchange_us_impl(g) +
+                                     sweep_us(*in, rmax, v == 1, v == 1 ? rmax : lds_rows_for(rmax)) +
+                                     0.3;
                     if (t < best) { best = t; grid = g; variant = v; }
                 }
                 if (g >= max_grid) break;
@@ -449,7 +480,8 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     }
     if (grid < 1) grid = 1;
     const int rmax = (a.N + grid - 1) / grid;
-    size_t lds = lds_bytes_for(*in, rmax, variant == 1);
+    const int lds_rows = variant == 1 ? 0 : lds_rows_for(rmax);
+    size_t lds = lds_bytes_for(*in, rmax, variant == 1) + (size_t)lds_rows * row_bytes;
     if (lds > (size_t)max_lds) return hipErrorInvalidValue;
     // More than half of the CU's LDS keeps one workgroup per CU, so the
     // grid spreads over every CU instead of doubling up on some.
@@ -484,6 +516,7 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     plan->variant = variant;
     plan->kslots = in->k;
     plan->block_m = in->m;
+    plan->lds_rows = lds_rows;
     plan->lds_bytes = lds;
     return hipSuccess;
 }
@@ -500,6 +533,7 @@ hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s
     TrainArgs args = a;
     args.grid = plan.grid;
     args.slot_spread = plan.slot_spread;
+    args.lds_rows = plan.variant ? 0 : plan.lds_rows;
     TrainKernel fn = plan.variant ? in->lds : in->stream;
     void *params[] = {&args};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),

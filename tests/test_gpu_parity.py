@@ -445,6 +445,21 @@ def test_streamed_variant_with_leading_rows_in_lds(rows, cols, d, n, epochs, lds
     assert plan["variant"] == 2 and plan["grid"] == 8
 
 
+@pytest.mark.parametrize("lds_rows", ["0", "1", "2", "64"])
+@pytest.mark.parametrize("rows,cols,d,n,epochs", [(6, 5, 3000, 30, 2), (5, 4, 9000, 20, 1)])
+def test_blocked_streamed_variant_with_leading_rows_in_lds(rows, cols, d, n, epochs, lds_rows,
+                                                           monkeypatch):
+    # the streamed blocked kernel (rows too long for the pipelined one) keeps
+    # its first rows in LDS and streams the rest; 4 workgroups give 8 and 5
+    # rows each
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", "2")
+    monkeypatch.setenv("SOM_TRAIN_GRID", "4")
+    monkeypatch.setenv("SOM_TRAIN_LDS_ROWS", lds_rows)
+    say("blocked streamed + LDS rows", rows, cols, d, n, epochs, "lds_rows", lds_rows)
+    plan = _train_vs_oracle(rows, cols, d, n, epochs)
+    assert plan["variant"] == 0 and plan["grid"] == 4
+
+
 def test_misaligned_samples_train_like_aligned_ones():
     # X starting one float into an allocation (d % 4 == 0 but rows not
     # 16-byte aligned) goes through the padded copy; results are bitwise
