@@ -159,8 +159,8 @@ __device__ inline float dot4(f4 a, f4 b, float acc) {
 // One pass of a sweeper over the workgroup's R rows, on its slices.  MAT
 // materialises w <- beta w + sum_i gamma_i xp_i from coef_prev; then with
 // z = xc_0 and f = w - z it accumulates f.f, f.(xc_i - z) for i >= 1 (ADOT)
-// and f.(xn_j - z) (BDOT), reduced over the wave into
-// dots[(r * 3 + sweeper) * 2M + ...] (complete in lane 63).  Rows (and their
+// and f.(xn_j - z) (BDOT), the last two as f.x - f.z of sums over the wave,
+// into dots[(r * 3 + sweeper) * 2M + ...] (written by lane 63).  Rows (and their
 // coefficients) are loaded D rows ahead, into a ring of registers indexed
 // statically.  Callers sweeping a part of the rows pass coef_prev and dots
 // advanced to its first row.
@@ -171,6 +171,7 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
     if (R <= 0) return;
     constexpr int ND = 2 * M;
     constexpr bool DOTS = ADOT || BDOT;
+    constexpr int NA = ND + 1;  // f.f, f.x_i, f.xn_j and f.z (last)
     row_t<LDSW> *rows = rows_as<LDSW>(rows_p);
     const int lane = threadIdx.x & 63, s = threadIdx.x >> 6;
     f4 ring[D][KS];
@@ -198,9 +199,9 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
         for (int u = 0; u < D; ++u) {
             const int r = rb + u;
             if (r < R) {
-                float acc[ND];
+                float acc[NA];
 #pragma unroll
-                for (int t = 0; t < ND; ++t) acc[t] = 0.f;
+                for (int t = 0; t < NA; ++t) acc[t] = 0.f;
                 // slices t >= nw hold zeros in w and in the samples
 #pragma unroll
                 for (int t = 0; t < KS; ++t) {
@@ -219,27 +220,37 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
                             if (t < nw) rows[(size_t)r * P4 + 64 * (s + kSweepers * t) + lane] = w;
                         }
                         if (DOTS) {
+                            // f.(x - z) as f.x - f.z after the lane sums:
+                            // the centring costs one dot per row instead of
+                            // a subtraction per sample and column
                             const f4 z = xc[0][t];
                             const f4 f = w - z;
                             acc[0] = dot4(f, f, acc[0]);
+                            acc[ND] = dot4(f, z, acc[ND]);
                             if (ADOT) {
 #pragma unroll
-                                for (int i = 1; i < M; ++i) acc[i] = dot4(f, xc[i][t] - z, acc[i]);
+                                for (int i = 1; i < M; ++i) acc[i] = dot4(f, xc[i][t], acc[i]);
                             }
                             if (BDOT) {
 #pragma unroll
                                 for (int j = 0; j < M; ++j)
-                                    acc[M + j] = dot4(f, xn[j][t] - z, acc[M + j]);
+                                    acc[M + j] = dot4(f, xn[j][t], acc[M + j]);
                             }
                         }
                     }
                 }
                 issue(r + D, ring[u], cring[u]);
                 if (DOTS) {
-                    wave_sums_last<ND>(acc);
-                    if (lane == 63)
+                    wave_sums_last<NA>(acc);
+                    if (lane == 63) {
+                        float *dr = dots + (r * kSweepers + s) * ND;
+                        dr[0] = acc[0];
 #pragma unroll
-                        for (int t = 0; t < ND; ++t) dots[(r * kSweepers + s) * ND + t] = acc[t];
+                        for (int t = 1; t < ND; ++t) {
+                            const bool used = t < M ? ADOT : BDOT;
+                            dr[t] = used ? acc[t] - acc[ND] : 0.f;
+                        }
+                    }
                 }
             }
         }
