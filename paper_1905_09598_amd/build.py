@@ -20,8 +20,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libsom.so")
-SOURCES = ["som_api.cpp", "som_train.hip", "som_train_pipe.hip", "som_eval.hip", "som_util.hip",
-           "som_pca.hip", "som_sparse.hip", "som_batch.hip"]
+SOURCES = ["som_api.cpp", "som_train.hip", "som_train_pipe.hip", "som_train_pipe_stream.hip",
+           "som_eval.hip", "som_util.hip", "som_pca.hip", "som_sparse.hip", "som_batch.hip"]
 ARCH = "gfx950"
 
 
@@ -40,10 +40,28 @@ def common_flags() -> list:
             f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
+# Translation units whose grid-exchange polls keep several loads in flight
+# (som_device.h, poll_slots).  Left structured, the poll loop's uniform early
+# exits are folded into the loop latch, and the merged path makes the
+# compiler wait for every poll in flight at each check; skipping the
+# structurization of uniform regions (their branches need no exec-mask
+# bookkeeping) keeps the exits as real exits.  The streamed pipelined
+# kernels (som_train_pipe_stream.hip) and the sparse kernel poll one load at
+# a time and are built without it.
+UNIFORM_EXIT_SOURCES = ("som_train.hip", "som_train_pipe.hip")
+
+
+def unit_flags(src: str) -> list:
+    if src in UNIFORM_EXIT_SOURCES:
+        return ["-mllvm", "-structurizecfg-skip-uniform-regions=true"]
+    return []
+
+
 def _compile(src: str) -> str:
     os.makedirs(BUILD, exist_ok=True)
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc()] + common_flags() + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = ([hipcc()] + common_flags() + unit_flags(src)
+           + ["-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj])
     r = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     err = "\n".join(l for l in r.stderr.splitlines() if noise not in l)
@@ -55,7 +73,7 @@ def _compile(src: str) -> str:
 
 
 def build(verbose: bool = True) -> str:
-    with ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
+    with ThreadPoolExecutor(max_workers=min(5, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs

@@ -6,6 +6,7 @@
 #include "som_internal.h"
 
 #include <math.h>
+#include <type_traits>
 
 namespace som {
 namespace dev {
@@ -262,44 +263,137 @@ __device__ inline void exchange_publish(const TrainArgs &a, int64_t e, unsigned 
     }
 }
 
+// Poll the slots base + lane + 64 k (k < K) of one exchange until every
+// lane has the key of each of its slots that exists, folding the keys into
+// m.  P polls per lane (4 or 8) are in flight, position q reading slot
+// q % K, so all of a group's slots are read in the same memory round trip
+// and each check waits only for the oldest poll, whose replacement goes out
+// right after it.  Control flow stays wave-uniform (the wave leaves once no
+// lane misses a key): per-lane exits would make the compiler copy the
+// in-flight values, and every copy waits for its load.  The positions are
+// unrolled by hand so that each exit is a plain break, and the translation
+// units that use this are built with uniform regions left unstructured;
+// exits merged into the loop latch would make the compiler wait for every
+// poll at the loop head.  Returns 0, or 1 if the map's status word turned
+// non-zero, or 2 on timeout.
+template <int q>
+using Pos = std::integral_constant<int, q>;
+
+template <int K, int P>
+__device__ inline int poll_slots(const TrainArgs &a, const unsigned long long *slots, int base,
+                                 unsigned tag, unsigned long long &m) {
+    static_assert(P == 4 || P == 8, "four or eight polls in flight");
+    const int lane = threadIdx.x & 63, G = a.grid, sp = a.slot_spread;
+    const unsigned long long *adr[K];
+    unsigned need = 0;
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+        const int i = base + lane + 64 * k;
+        const bool mine = i < G;
+        adr[k] = slots + (int64_t)(mine ? i : base) * sp;
+        need |= mine ? 1u << k : 0u;
+    }
+    unsigned long long v[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q)
+        v[q] = __hip_atomic_load(adr[q % K], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // Check position q and put its next poll in flight (before the exit
+    // test: a poll skipped on the way out would leave the loop head unsure
+    // which load is the oldest); true once no lane misses a key.
+    const auto step = [&](auto pos) {
+        constexpr int q = decltype(pos)::value;
+        constexpr unsigned bit = 1u << (q % K);
+        const bool ok = (need & bit) != 0 && ((unsigned)(v[q] >> kUnitBits) & 0xffu) == tag;
+        m = ok ? u64_min(m, v[q]) : m;
+        need &= ok ? ~bit : ~0u;
+        const bool done = __ballot(need != 0) == 0;
+        v[q] = __hip_atomic_load(adr[q % K], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return done;
+    };
+    const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+    int r = 0;
+    for (unsigned spins = 1;; ++spins) {
+        if ((spins & 15u) == 0) {
+            const int32_t st =
+                __hip_atomic_load(&a.state->status, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (__ballot(st != 0) != 0) {
+                r = 1;
+                break;
+            }
+            if (__builtin_amdgcn_s_memrealtime() - t0 > a.timeout_ticks) {
+                r = 2;
+                break;
+            }
+        }
+        if (step(Pos<0>{})) break;
+        if (step(Pos<1>{})) break;
+        if (step(Pos<2>{})) break;
+        if (step(Pos<3>{})) break;
+        if constexpr (P == 8) {
+            if (step(Pos<4>{})) break;
+            if (step(Pos<5>{})) break;
+            if (step(Pos<6>{})) break;
+            if (step(Pos<7>{})) break;
+        }
+    }
+    return r;
+}
+
 // Wait for every workgroup's key of exchange e and return the winning unit
 // (the same in all lanes), or -1 if the wait was given up.  `best` is this
-// workgroup's own key (the answer when the grid is one workgroup).
+// workgroup's own key (the answer when the grid is one workgroup).  P polls
+// per lane are kept in flight: 4 or 8, or 1 (each lane waits for its slots
+// one after the other: the fewest registers and the least polling traffic).
+template <int P>
 __device__ inline int exchange_wait(const TrainArgs &a, int64_t e, unsigned long long best) {
     const int lane = threadIdx.x & 63, G = a.grid;
     if (G == 1) return (int)(best & (unsigned long long)kMaxUnits);
     const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
-    const int sp = a.slot_spread;
-    const int64_t par = (e & 1) * (int64_t)G * sp;
+    const int64_t par = (e & 1) * (int64_t)G * a.slot_spread;
     const unsigned long long *slots =
         a.slots + (blockIdx.x % kSlotReplicas) * kSlotReplicaStride + par;
     unsigned long long m = ~0ull;
     int abort = 0;
-    for (int i = lane; i < G && !abort; i += 64) {
-        const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
-        unsigned spins = 0;
-        for (;;) {
-            const unsigned long long v = __hip_atomic_load(slots + (int64_t)i * sp, __ATOMIC_RELAXED,
-                                                           __HIP_MEMORY_SCOPE_AGENT);
-            if (((unsigned)(v >> kUnitBits) & 0xffu) == tag) {
-                m = u64_min(m, v);
-                break;
-            }
-            if ((++spins & 63u) == 0) {
-                if (__hip_atomic_load(&a.state->status, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT) != 0) {
-                    abort = 1;
+    if constexpr (P == 1) {
+        // One poll per lane at a time, each lane waiting for its slots one
+        // after the other: the fewest registers.
+        const int sp = a.slot_spread;
+        for (int i = lane; i < G && abort == 0; i += 64) {
+            const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+            for (unsigned spins = 1;; ++spins) {
+                const unsigned long long v = __hip_atomic_load(
+                    slots + (int64_t)i * sp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (((unsigned)(v >> kUnitBits) & 0xffu) == tag) {
+                    m = u64_min(m, v);
                     break;
                 }
-                if (__builtin_amdgcn_s_memrealtime() - t0 > a.timeout_ticks) {
-                    __hip_atomic_store(&a.state->status, kStatusTimeout, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-                    abort = 1;
-                    break;
+                if ((spins & 63u) == 0) {
+                    if (__hip_atomic_load(&a.state->status, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT) != 0) {
+                        abort = 1;
+                        break;
+                    }
+                    if (__builtin_amdgcn_s_memrealtime() - t0 > a.timeout_ticks) {
+                        abort = 2;
+                        break;
+                    }
                 }
             }
         }
+    } else {
+        for (int base = 0; base < G && abort == 0; base += 256) {
+            const int left = G - base;
+            abort = left <= 64    ? poll_slots<1, P>(a, slots, base, tag, m)
+                    : left <= 128 ? poll_slots<2, P>(a, slots, base, tag, m)
+                                  : poll_slots<4, P>(a, slots, base, tag, m);
+        }
     }
+    // The timeout is recorded after the polls: a store among them would mix
+    // stores into the loads in flight, and the compiler then waits for every
+    // poll at each check.
+    if (abort == 2)
+        __hip_atomic_store(&a.state->status, kStatusTimeout, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     // With at most 64 workgroups lane i holds workgroup i's key, and
     // workgroups own increasing unit ranges.
     m = wave_min_key(m, G <= 64);
@@ -312,9 +406,10 @@ __device__ inline int exchange_wait(const TrainArgs &a, int64_t e, unsigned long
 // up.  Each workgroup writes its key into every XCD's copy of the slot
 // array and polls the copy of its own XCD; slots alternate by the parity
 // of e and carry a tag of e, so a slot is never read for the wrong step.
+template <int P>
 __device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long best) {
     exchange_publish(a, e, best);
-    return exchange_wait(a, e, best);
+    return exchange_wait<P>(a, e, best);
 }
 
 // Neighbourhood factor of owned row r given BMU c: lr * 2^(-g * c2) with g
@@ -347,8 +442,9 @@ __device__ inline float neighbour_h(const TrainArgs &a, float4 p, float cr, floa
 // (1 - h) and sets gam_k = h, so
 //   quad <- (1 - h)^2 quad + 2 h (1 - h) lin_k + h^2 E_kk,
 //   lin_l <- (1 - h) lin_l + h E_kl.
-// Returns false if an exchange was given up.
-template <int M>
+// Returns false if an exchange was given up.  P: polls in flight per lane
+// in each exchange.
+template <int M, int P>
 __device__ inline bool block_steps(const TrainArgs &a, int64_t s0, int mb, int r0, int R,
                                    const float (&E)[M * (M + 1) / 2], float4 p, float inv_cols,
                                    StepWindow<float2> &sw, float &beta, float (&gam)[M]) {
@@ -370,7 +466,7 @@ __device__ inline bool block_steps(const TrainArgs &a, int64_t s0, int mb, int r
         const float D = fmaf(-2.f, lin[k], Ekk) + quad;
         const unsigned long long best =
             wave_argmin_key(lane < R ? dist_order_bits(D) : 0xffffffffu, r0);
-        const int c = exchange(a, s, best);
+        const int c = exchange<P>(a, s, best);
         if (c < 0) {
             ok = false;
             continue;

@@ -178,6 +178,10 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
                                   StepWindow<float2> &sw) {
     constexpr int T = M * (M + 1) / 2;
     constexpr int WPR = L / 64;
+    // Polls in flight per exchange.  One-wave workgroups hold their sample
+    // blocks across the exchange, and one poll at a time keeps those in
+    // registers.
+    constexpr int kPolls = L == 64 ? 1 : 8;
     const int lane = threadIdx.x & 63;
     const float inv_cols = 1.f / (float)a.cols;
     if (WPR > 1) {
@@ -195,7 +199,7 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
 #pragma unroll
         for (int t = 0; t < T; ++t) Er[t] = lane < R ? E[lane * T + t] : 0.f;
         if (lane < R) p = pos[lane];
-        const bool ok = block_steps<M>(a, s0, mb, r0, R, Er, p, inv_cols, sw, beta, gam);
+        const bool ok = block_steps<M, kPolls>(a, s0, mb, r0, R, Er, p, inv_cols, sw, beta, gam);
         if (lane < R) {
             coef[lane * (M + 1)] = beta;
 #pragma unroll
@@ -229,7 +233,7 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
             best = u64_min(best, row_key(D, r0 + r));
         }
         best = wave_min_key(best, false);
-        const int c = exchange(a, s, best);
+        const int c = exchange<kPolls>(a, s, best);
         if (c < 0) return false;
         if (blockIdx.x == 0 && lane == 0 && a.bmu_trace) a.bmu_trace[s] = c;
         const float2 sc = sw.get(a, s);

@@ -1,487 +1,30 @@
-// Pipelined online-SOM training kernel for gfx950 (MI355X): the pass over
-// the prototypes runs concurrently with the grid exchanges.
-//
-// The training of som_train.hip alternates two phases per block of M steps:
-// wave 0 finds the block's M BMUs (M grid exchanges), then every wave sweeps
-// the prototypes once.  Here wave 3 (the controller) runs the exchanges of
-// block b while waves 0-2 (the sweepers) already sweep for block b + 1, so a
-// step costs about one exchange instead of one exchange plus a share of the
-// sweep.  What makes this possible is that block b + 1's Gram matrices need
-// block b's coefficients only through scalars:
-//
-//   F_b      prototype at the start of block b (materialised in memory/LDS),
-//   z        a centring vector, the first sample of block b,
-//   f        = F_b - z,   A_i = x_{b,i} - z,   B_j = x_{b+1,j} - z,
-//   F_{b+1}  = beta F_b + sum_i gamma_i x_{b,i}   (beta + sum_i gamma_i = 1)
-//   e_j      = x_{b+1,j} - F_{b+1} = B_j - beta f - sum_i gamma_i A_i
-//   E_{b+1}[j,l] = e_j . e_l
-//            = B_j.B_l - P_j - P_l + Q,
-//   P_j      = beta f.B_j + sum_i gamma_i A_i.B_j,
-//   Q        = beta^2 f.f + 2 beta sum_i gamma_i f.A_i + sum_ik gamma_i gamma_k A_i.A_k.
-//
-// Per unit the sweep of block b needs only F_b and the samples: it
-// materialises F_b from F_{b-1} with block b-1's coefficients (known when
-// block b starts) and accumulates f.f, f.A_i and f.B_j.  The sample-sample
-// products A.A, A.B and B.B are the same for every unit and come from a
-// prepass over the blocks.  The controller then forms E_{b+1} from these
-// scalars and block b's coefficients.  Centring on a sample keeps every term
-// at the scale of sample-to-prototype distances.
-//
-// The sweepers split the columns, not the rows: sweeper s owns the 64-column
-// float4 slices s, s + 3, s + 6, ... of every row and keeps its slices of the
-// samples of blocks b - 1, b and b + 1 in registers, so a row visit reads
-// and writes only the row itself.  Each sweeper reduces its partial dot
-// products over its lanes and the controller adds the three partials.  Rows
-// are loaded a few rows ahead of their use.  The next block's samples are
-// loaded at the end of a sweep, while the sweepers wait for the controller.
-// The samples stay raw (centred per use, as the prepass does), so that a
-// unit rate with a zero radius still copies a sample bit-exactly.
-#include "som_device.h"
+// Pipelined online-SOM training: the LDS-resident instances of the kernel
+// in som_train_pipe.h, the launch planner and the launcher.
+#include "som_train_pipe.h"
 
 namespace som {
 namespace {
 
 using namespace dev;
 
-constexpr int kSweepers = 3;    // waves 0..2 sweep
-constexpr int kController = 3;  // wave 3 runs the exchanges
-constexpr int kPipeHeader = 64;
-
-template <int M>
-constexpr int dots_stride() { return M * (M + 1) + M * M; }  // AA (T), AB (M*M), BB (T)
-
-// ---------------------------------------------------------------- prepass
-// Per block b: z = x_{b,0}; A_i = x_{b,i} - z; B_j = x_{b+1,j} - z (samples
-// past the last step are sample 0, as in the training kernel).  Writes
-// out[b] = (A_i.A_k for i <= k, A_i.B_j row-major in i, B_j.B_l for j <= l).
-template <int M>
-__global__ __launch_bounds__(256) void block_dots_kernel(TrainArgs a, float *out,
-                                                         int64_t nblocks) {
-    constexpr int T = M * (M + 1) / 2;
-    constexpr int ND = dots_stride<M>();
-    __shared__ float red[4][ND];
-    const int64_t b = blockIdx.x;
-    if (b >= nblocks) return;
-    const float *xa[M], *xb[M];
-#pragma unroll
-    for (int j = 0; j < M; ++j) {
-        const int64_t sa = b * M + j, sb = (b + 1) * M + j;
-        int ia = sa < a.nsteps ? a.order[sa] : 0, ib = sb < a.nsteps ? a.order[sb] : 0;
-        ia = (ia >= 0 && (int64_t)ia < a.n) ? ia : 0;
-        ib = (ib >= 0 && (int64_t)ib < a.n) ? ib : 0;
-        xa[j] = a.X + (int64_t)ia * a.xld;
-        xb[j] = a.X + (int64_t)ib * a.xld;
-    }
-    float acc[ND];
-#pragma unroll
-    for (int t = 0; t < ND; ++t) acc[t] = 0.f;
-    for (int c = threadIdx.x; c < a.d; c += 256) {
-        const float z = xa[0][c];
-        float A[M], B[M];
-#pragma unroll
-        for (int j = 0; j < M; ++j) {
-            A[j] = xa[j][c] - z;
-            B[j] = xb[j][c] - z;
-        }
-#pragma unroll
-        for (int k = 0; k < M; ++k)
-#pragma unroll
-            for (int i = 0; i <= k; ++i) {
-                acc[tri(i, k)] = fmaf(A[i], A[k], acc[tri(i, k)]);
-                acc[T + M * M + tri(i, k)] = fmaf(B[i], B[k], acc[T + M * M + tri(i, k)]);
-            }
-#pragma unroll
-        for (int i = 0; i < M; ++i)
-#pragma unroll
-            for (int j = 0; j < M; ++j) acc[T + i * M + j] = fmaf(A[i], B[j], acc[T + i * M + j]);
-    }
-    wave_sums<ND>(acc);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (lane == 0)
-#pragma unroll
-        for (int t = 0; t < ND; ++t) red[wave][t] = acc[t];
-    __syncthreads();
-    for (int t = threadIdx.x; t < ND; t += 256)
-        out[b * ND + t] = (red[0][t] + red[1][t]) + (red[2][t] + red[3][t]);
-}
-
-// ---------------------------------------------------------------- layout
-struct PipeLayout {
-    int Rp;
-    float *dots;   // 2 parities x Rp rows x 3 sweepers x 2M
-    float *coef;   // 2 parities x Rp x (M + 1)
-    float4 *pos;   // Rp
-    f4 *lw;        // R x P4 (LDS variant)
-};
-
-template <int M>
-__device__ inline PipeLayout pipe_layout(unsigned char *smem, int R) {
-    PipeLayout l;
-    l.Rp = (R + 3) & ~3;
-    unsigned char *p = smem + kPipeHeader;
-    l.dots = reinterpret_cast<float *>(p);
-    p += (size_t)2 * l.Rp * kSweepers * 2 * M * 4;
-    l.coef = reinterpret_cast<float *>(p);
-    p += (size_t)2 * l.Rp * (M + 1) * 4;
-    p = reinterpret_cast<unsigned char *>((reinterpret_cast<uintptr_t>(p) + 15) & ~(uintptr_t)15);
-    l.pos = reinterpret_cast<float4 *>(p);
-    p += (size_t)l.Rp * 16;
-    l.lw = reinterpret_cast<f4 *>(p);
-    return l;
-}
-
-// ---------------------------------------------------------------- sweepers
-// Sweeper slices: wave s owns slices s + 3t, t < nw (nw <= KS).
-__device__ inline int sweeper_slices(int nsl) {
-    const int s = threadIdx.x >> 6;
-    return nsl > s ? (nsl - s + kSweepers - 1) / kSweepers : 0;
-}
-
-// This wave's slices of the M samples of block blk (steps past the end load
-// sample 0; columns past d, and slices t >= nw, are zero).
-template <int M, int KS>
-__device__ inline void load_samples(f4 (&x)[M][KS], const TrainArgs &a, int64_t blk,
-                                    StepWindow<int> &ow) {
-    const int lane = threadIdx.x & 63, s = threadIdx.x >> 6;
-#pragma unroll
-    for (int j = 0; j < M; ++j) {
-        const int64_t st = blk * M + j;
-        const int i = st < a.nsteps ? ow.get(a, st) : 0;
-#pragma unroll
-        for (int t = 0; t < KS; ++t) x[j][t] = sample_f4(a, i, 64 * (s + kSweepers * t) + lane);
-    }
-}
-
-__device__ inline float dot4(f4 a, f4 b, float acc) {
-    return fmaf(a.x, b.x, fmaf(a.y, b.y, fmaf(a.z, b.z, fmaf(a.w, b.w, acc))));
-}
-
-// One pass of a sweeper over the workgroup's R rows, on its slices.  MAT
-// materialises w <- beta w + sum_i gamma_i xp_i from coef_prev; then with
-// z = xc_0 and f = w - z it accumulates f.f, f.(xc_i - z) for i >= 1 (ADOT)
-// and f.(xn_j - z) (BDOT), the last two as f.x - f.z of sums over the wave,
-// into dots[(r * 3 + sweeper) * 2M + ...] (written by lane 63).  Rows (and their
-// coefficients) are loaded D rows ahead, into a ring of registers indexed
-// statically.  Callers sweeping a part of the rows pass coef_prev and dots
-// advanced to its first row.
-template <int M, int KS, int D, bool LDSW, bool MAT, bool ADOT, bool BDOT>
-__device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&xp)[M][KS],
-                                  const f4 (&xc)[M][KS], const f4 (&xn)[M][KS],
-                                  const float *coef_prev, float *dots) {
-    if (R <= 0) return;
-    constexpr int ND = 2 * M;
-    constexpr bool DOTS = ADOT || BDOT;
-    constexpr int NA = ND + 1;  // f.f, f.x_i, f.xn_j and f.z (last)
-    row_t<LDSW> *rows = rows_as<LDSW>(rows_p);
-    const int lane = threadIdx.x & 63, s = threadIdx.x >> 6;
-    f4 ring[D][KS];
-    float cring[D][M + 1];
-    // Loads are unconditional (clamped row and column, unused or zeroed
-    // when out of range) so that a burst of them is waited for once.
-    auto issue = [&](int r, f4 (&dst)[KS], float (&cdst)[M + 1]) {
-        const int rr = r < R ? r : R - 1;
-#pragma unroll
-        for (int t = 0; t < KS; ++t) {
-            const int q = 64 * (s + kSweepers * t) + lane;
-            const f4 v = rows[(size_t)rr * P4 + (q < P4 ? q : P4 - 1)];
-            const f4 zero = {0.f, 0.f, 0.f, 0.f};
-            dst[t] = t < nw ? v : zero;
-        }
-        if (MAT) {
-#pragma unroll
-            for (int i = 0; i <= M; ++i) cdst[i] = coef_prev[rr * (M + 1) + i];
-        }
-    };
-#pragma unroll
-    for (int u = 0; u < D; ++u) issue(u, ring[u], cring[u]);
-    for (int rb = 0; rb < R; rb += D) {
-#pragma unroll
-        for (int u = 0; u < D; ++u) {
-            const int r = rb + u;
-            if (r < R) {
-                float acc[NA];
-#pragma unroll
-                for (int t = 0; t < NA; ++t) acc[t] = 0.f;
-                // slices t >= nw hold zeros in w and in the samples
-#pragma unroll
-                for (int t = 0; t < KS; ++t) {
-                    {
-                        f4 w = ring[u][t];
-                        if (MAT) {
-                            w = w * cring[u][0];
-#pragma unroll
-                            for (int i = 0; i < M; ++i) {
-                                const float g = cring[u][1 + i];
-                                w.x = fmaf(g, xp[i][t].x, w.x);
-                                w.y = fmaf(g, xp[i][t].y, w.y);
-                                w.z = fmaf(g, xp[i][t].z, w.z);
-                                w.w = fmaf(g, xp[i][t].w, w.w);
-                            }
-                            if (t < nw) rows[(size_t)r * P4 + 64 * (s + kSweepers * t) + lane] = w;
-                        }
-                        if (DOTS) {
-                            // f.(x - z) as f.x - f.z after the lane sums:
-                            // the centring costs one dot per row instead of
-                            // a subtraction per sample and column
-                            const f4 z = xc[0][t];
-                            const f4 f = w - z;
-                            acc[0] = dot4(f, f, acc[0]);
-                            acc[ND] = dot4(f, z, acc[ND]);
-                            if (ADOT) {
-#pragma unroll
-                                for (int i = 1; i < M; ++i) acc[i] = dot4(f, xc[i][t], acc[i]);
-                            }
-                            if (BDOT) {
-#pragma unroll
-                                for (int j = 0; j < M; ++j)
-                                    acc[M + j] = dot4(f, xn[j][t], acc[M + j]);
-                            }
-                        }
-                    }
-                }
-                issue(r + D, ring[u], cring[u]);
-                if (DOTS) {
-                    wave_sums_last<NA>(acc);
-                    if (lane == 63) {
-                        float *dr = dots + (r * kSweepers + s) * ND;
-                        dr[0] = acc[0];
-#pragma unroll
-                        for (int t = 1; t < ND; ++t) {
-                            const bool used = t < M ? ADOT : BDOT;
-                            dr[t] = used ? acc[t] - acc[ND] : 0.f;
-                        }
-                    }
-                }
-            }
-        }
-    }
-}
-
-// A sweep over the workgroup's R rows: rows [0, RL) from LDS (loaded two
-// ahead) and, in the streamed variant (LDSW false), rows [RL, R) from
-// memory at gs (loaded four ahead).
-template <int M, int KS, bool LDSW, bool MAT, bool ADOT, bool BDOT>
-__device__ inline void sweep_rows(f4 *lw, int RL, f4 *gs, int R, int P4, int nw,
-                                  const f4 (&xp)[M][KS], const f4 (&xc)[M][KS],
-                                  const f4 (&xn)[M][KS], const float *coef_prev, float *dots) {
-    constexpr int ND = 2 * M;
-    pipe_sweep<M, KS, 2, true, MAT, ADOT, BDOT>(lw, RL, P4, nw, xp, xc, xn, coef_prev, dots);
-    if constexpr (!LDSW)
-        pipe_sweep<M, KS, 4, false, MAT, ADOT, BDOT>(gs, R - RL, P4, nw, xp, xc, xn,
-                                                     coef_prev + (size_t)RL * (M + 1),
-                                                     dots + (size_t)RL * kSweepers * ND);
-}
-
-// ---------------------------------------------------------------- controller
-// Controller lane r (< R): Gram matrix E of the next block from the sweep's
-// products of row r (d: f.f, f.A_1.., f.B_0.., summed over the sweepers),
-// the previous block's coefficients (beta, gam) and the block's sample
-// products (AA, AB, BB of the previous block; for the first block BB = its
-// own AA).
-template <int M>
-__device__ inline void gram_from_dots(const float (&d)[2 * M], float beta, const float (&gam)[M],
-                                      const float (&AA)[M * (M + 1) / 2], const float (&AB)[M * M],
-                                      const float (&BB)[M * (M + 1) / 2],
-                                      float (&E)[M * (M + 1) / 2]) {
-    float P[M];
-    const float ff = d[0];
-#pragma unroll
-    for (int j = 0; j < M; ++j) {
-        float p = beta * d[M + j];
-#pragma unroll
-        for (int i = 0; i < M; ++i) p = fmaf(gam[i], AB[i * M + j], p);
-        P[j] = p;
-    }
-    float lin = 0.f, quad = 0.f;
-#pragma unroll
-    for (int i = 0; i < M; ++i) {
-        float inner = 0.f;
-#pragma unroll
-        for (int k = 0; k < M; ++k) inner = fmaf(gam[k], AA[tri_any(i, k)], inner);
-        if (i > 0) lin = fmaf(gam[i], d[i], lin);
-        quad = fmaf(gam[i], inner, quad);
-    }
-    const float Q = fmaf(beta * beta, ff, fmaf(2.f * beta, lin, quad));
-#pragma unroll
-    for (int l = 0; l < M; ++l)
-#pragma unroll
-        for (int j = 0; j <= l; ++j) E[tri(j, l)] = BB[tri(j, l)] - P[j] - P[l] + Q;
-}
-
-// The sample products of block blk, spread over the lanes: entry t is held
-// by lane t % 64 of word t / 64.
-template <int M>
-struct SampleDots {
-    static constexpr int N = dots_stride<M>();
-    static constexpr int W = (N + 63) / 64;
-    float v[W];
-    __device__ void load(const float *sdots, int64_t blk, int64_t nblocks) {
-        const int lane = threadIdx.x & 63;
-#pragma unroll
-        for (int w = 0; w < W; ++w) {
-            const int t = 64 * w + lane;
-            v[w] = (t < N && blk < nblocks) ? sdots[blk * N + t] : 0.f;
-        }
-    }
-    __device__ float at(int t) const { return lane_f(v[t / 64], t % 64); }
-};
-
-template <int M, int KS, bool LDSW>
-__global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
-    constexpr int T = M * (M + 1) / 2;
-    constexpr int ND = 2 * M;
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int G = a.grid, b = blockIdx.x, tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63;
-    const int r0 = (int)(((int64_t)b * a.N) / G);
-    const int r1 = (int)(((int64_t)(b + 1) * a.N) / G);
-    const int R = r1 - r0;  // 1 <= R <= 64 (planner)
-    const int P4 = (int)(a.ld / 4);
-    const int nw = sweeper_slices(P4 / 64);  // <= KS (planner)
-    const float inv_cols = 1.f / (float)a.cols;
-    Bcast *bc = reinterpret_cast<Bcast *>(smem);
-    const PipeLayout l = pipe_layout<M>(smem, R);
-
-    if (a.state->order_bad) return;  // same value for every workgroup
-    if (a.nsteps <= 0) return;
-
-    for (int r = tid; r < R; r += 256) {
-        const int u = r0 + r, ur = u / a.cols, uc = u - ur * a.cols;
-        l.pos[r] = make_float4((float)ur, (float)uc, (float)(ur & 1), 0.f);
-    }
-    if (tid == 0) bc->abort = 0;
-    f4 *gw = reinterpret_cast<f4 *>(a.W) + (int64_t)r0 * P4;
-    // Rows [0, RL) live in LDS for the whole launch; the streamed variant
-    // keeps as many as its LDS holds (planner) and streams the rest.
-    const int RL = LDSW ? R : (a.lds_rows < R ? (a.lds_rows > 0 ? a.lds_rows : 0) : R);
-    if (RL > 0) {
-        row_t<true> *lw = rows_as<true>(l.lw);
-        const row_t<false> *g = rows_as<false>(gw);
-        for (int e = tid; e < RL * P4; e += 256) lw[e] = g[e];
-    }
-    f4 *gs = gw + (int64_t)RL * P4;  // first streamed row
-    const int64_t nb = (a.nsteps + M - 1) / M;
-    __syncthreads();
-    // The controller and the sweepers run separate loops over the blocks that
-    // meet at one barrier per block (and one before the first), so that each
-    // keeps only its own state in registers.
-    if (wave == kController) {
-        StepWindow<float2> sw;
-        sw.init(a, 0);
-        float beta_prev = 1.f, gam_prev[M];
-#pragma unroll
-        for (int j = 0; j < M; ++j) gam_prev[j] = 0.f;
-        const float4 p = lane < R ? l.pos[lane] : make_float4(0.f, 0.f, 0.f, 0.f);
-        SampleDots<M> sd;
-        sd.load(a.block_dots, 0, nb);
-        __syncthreads();  // the sweepers' products of the initial prototypes
-        for (int64_t blk = 0; blk < nb; ++blk) {
-            const int par = (int)(blk & 1);
-            float AA[T], AB[M * M], BB[T], E[T], d[ND];
-#pragma unroll
-            for (int t = 0; t < T; ++t) AA[t] = sd.at(t);
-#pragma unroll
-            for (int t = 0; t < M * M; ++t) AB[t] = sd.at(T + t);
-#pragma unroll
-            for (int t = 0; t < T; ++t) BB[t] = blk == 0 ? AA[t] : sd.at(T + M * M + t);
-            const float *dr =
-                l.dots + ((size_t)(par ^ 1) * l.Rp + (lane < R ? lane : 0)) * kSweepers * ND;
-#pragma unroll
-            for (int t = 0; t < ND; ++t) d[t] = (dr[t] + dr[ND + t]) + dr[2 * ND + t];
-            if (blk == 0) {
-                // the initial prototypes' products with block 0 itself:
-                // f.B_j = f.A_j (B_0 = A_0 = 0)
-                d[M] = 0.f;
-#pragma unroll
-                for (int j = 1; j < M; ++j) d[M + j] = d[j];
-            }
-            gram_from_dots<M>(d, beta_prev, gam_prev, AA, AB, BB, E);
-            if (blk + 1 < nb) sd.load(a.block_dots, blk, nb);
-            const int64_t s0 = blk * M;
-            const int mb = (int)((a.nsteps - s0) < M ? (a.nsteps - s0) : M);
-            float beta, gam[M];
-            const bool ok = block_steps<M>(a, s0, mb, r0, R, E, p, inv_cols, sw, beta, gam);
-            if (lane < R) {
-                float *cf = l.coef + ((size_t)par * l.Rp + lane) * (M + 1);
-                cf[0] = beta;
-#pragma unroll
-                for (int j = 0; j < M; ++j) cf[1 + j] = gam[j];
-            }
-            beta_prev = beta;
-#pragma unroll
-            for (int j = 0; j < M; ++j) gam_prev[j] = gam[j];
-            if (!ok && lane == 0) bc->abort = 1;
-            __syncthreads();
-            if (!ok) return;  // the sweepers read it from bc->abort
-        }
-    } else {
-        StepWindow<int> own;
-        own.init(a, 0);
-        // Slices of the samples of the previous, current and next block.
-        f4 xp[M][KS], xc[M][KS], xn[M][KS];
-        load_samples<M, KS>(xc, a, 0, own);
-        if (nb > 1) load_samples<M, KS>(xn, a, 1, own);
-        // Products of the initial prototypes with block 0 (centred on its
-        // first sample): f.f and f.(x_{0,i} - z), parity 1.
-        sweep_rows<M, KS, LDSW, false, true, false>(l.lw, RL, gs, R, P4, nw, xc, xc, xc, l.coef,
-                                                 l.dots + (size_t)l.Rp * kSweepers * ND);
-        __syncthreads();
-        for (int64_t blk = 0; blk < nb; ++blk) {
-            const int par = (int)(blk & 1);
-            const float *cp = l.coef + (size_t)(par ^ 1) * l.Rp * (M + 1);
-            float *dd = l.dots + (size_t)par * l.Rp * kSweepers * ND;
-            const bool has_next = blk + 1 < nb;
-            if (blk == 0) {
-                if (has_next)
-                    sweep_rows<M, KS, LDSW, false, true, true>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp, dd);
-            } else if (has_next) {
-                sweep_rows<M, KS, LDSW, true, true, true>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp, dd);
-            } else {
-                sweep_rows<M, KS, LDSW, true, false, false>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp, dd);
-            }
-#pragma unroll
-            for (int j = 0; j < M; ++j)
-#pragma unroll
-                for (int t = 0; t < KS; ++t) {
-                    xp[j][t] = xc[j][t];
-                    xc[j][t] = xn[j][t];
-                }
-            if (blk + 2 < nb) load_samples<M, KS>(xn, a, blk + 2, own);
-            __syncthreads();
-            if (bc->abort) return;
-        }
-        // apply the last block's updates
-        sweep_rows<M, KS, LDSW, true, false, false>(
-            l.lw, RL, gs, R, P4, nw, xp, xc, xn, l.coef + (size_t)((nb - 1) & 1) * l.Rp * (M + 1),
-            l.dots);
-    }
-    if (RL > 0) {
-        __syncthreads();
-        const row_t<true> *lw = rows_as<true>(l.lw);
-        row_t<false> *g = rows_as<false>(gw);
-        for (int e = tid; e < RL * P4; e += 256) g[e] = lw[e];
-    }
-}
-
-typedef void (*PipeKernel)(TrainArgs);
 typedef void (*DotsKernel)(TrainArgs, float *, int64_t);
 
 struct PipeInstance {
     int m, ks;
     bool stream_ok;  // the streamed variant fits in registers
-    PipeKernel stream, lds;
+    PipeKernel lds;
     DotsKernel dots;
 };
 
 template <int M, int KS, bool STREAM = true>
 constexpr PipeInstance pipe_instance() {
-    return PipeInstance{M, KS, STREAM, STREAM ? train_pipe_kernel<M, KS, false> : nullptr,
-                        train_pipe_kernel<M, KS, true>, block_dots_kernel<M>};
+    return PipeInstance{M, KS, STREAM, train_pipe_kernel<M, KS, true>, block_dots_kernel<M>};
 }
 
 // (M, KS): block length and float4 slices of 64 columns per sweeper (rows of
 // up to 3 * 64 * KS float4).  The sample registers, 3 M KS float4 per lane,
-// bound M * KS; with KS = 7 only the LDS variant stays out of scratch.
+// bound M * KS; with KS = 7 only the LDS variant stays out of scratch.  The
+// streamed kernels of the same shapes are listed in som_train_pipe_stream.hip.
 const PipeInstance kPipe[] = {pipe_instance<8, 1>(), pipe_instance<4, 1>(), pipe_instance<4, 2>(),
                               pipe_instance<4, 3>(), pipe_instance<2, 3>(), pipe_instance<2, 4>(),
                               pipe_instance<2, 7, false>()};
@@ -566,9 +109,10 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
         plan->block = 256;
         plan->slot_spread = plan->grid <= 64 ? 16 : 4;
         const PipeInstance *pi = pipe_for(plan->block_m, plan->kslots);
-        PipeKernel fn = plan->variant == 3 ? pi->lds : pi->stream;
+        PipeKernel fn = plan->variant == 3 ? pi->lds : pipe_stream_kernel(pi->m, pi->ks);
         int per_cu = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        if (!fn ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(
                 &per_cu, reinterpret_cast<const void *>(fn), 256, plan->lds_bytes) != hipSuccess ||
             per_cu < 1 || plan->grid > per_cu * num_cus || plan->grid > kMaxTrainGrid)
             return 1e300;
@@ -596,7 +140,7 @@ hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStrea
     pi->dots<<<dim3((unsigned)nb), dim3(256), 0, s>>>(args, args.block_dots, nb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    PipeKernel fn = plan.variant == 3 ? pi->lds : pi->stream;
+    PipeKernel fn = plan.variant == 3 ? pi->lds : pipe_stream_kernel(pi->m, pi->ks);
     if (!fn) return hipErrorInvalidValue;
     void *params[] = {&args};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),

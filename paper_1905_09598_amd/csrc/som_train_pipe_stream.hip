@@ -1,0 +1,27 @@
+// Streamed-prototype instances of the pipelined training kernel of
+// som_train_pipe.h.  They sit in a translation unit of their own because
+// they are compiled without the structurizer option of the LDS-resident
+// instances: in the streamed sweep it raises register pressure enough to
+// cost more than the faster exchange polling it buys (see build.py).
+#include "som_train_pipe.h"
+
+namespace som {
+
+PipeKernel pipe_stream_kernel(int m, int ks) {
+    struct Entry {
+        int m, ks;
+        PipeKernel fn;
+    };
+    // The shapes of the LDS-resident table whose sample registers leave
+    // room for streamed rows (not KS = 7).
+    static const Entry kStream[] = {
+        {8, 1, train_pipe_kernel<8, 1, false>}, {4, 1, train_pipe_kernel<4, 1, false>},
+        {4, 2, train_pipe_kernel<4, 2, false>}, {4, 3, train_pipe_kernel<4, 3, false>},
+        {2, 3, train_pipe_kernel<2, 3, false>}, {2, 4, train_pipe_kernel<2, 4, false>},
+    };
+    for (const Entry &e : kStream)
+        if (e.m == m && e.ks == ks) return e.fn;
+    return nullptr;
+}
+
+}  // namespace som
