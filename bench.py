@@ -35,7 +35,8 @@ FP32_MFMA_PEAK_TFLOPS = 157.3
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "train_kernel_traffic.json")
 TRAIN_SOURCES = [os.path.join(ROOT, "paper_1905_09598_amd", "csrc", f)
                  for f in ("som_device.h", "som_internal.h", "som_train.hip",
-                           "som_train_pipe.hip")]
+                           "som_train_pipe.h", "som_train_pipe.hip",
+                           "som_train_pipe_stream.hip")]
 
 
 def kernel_source_sha() -> str:
