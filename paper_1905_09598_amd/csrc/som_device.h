@@ -279,6 +279,10 @@ __device__ inline void exchange_publish(const TrainArgs &a, int64_t e, unsigned 
 template <int q>
 using Pos = std::integral_constant<int, q>;
 
+// s_waitcnt immediate for vmcnt(0) with the other counters left alone
+// (expcnt 7, lgkmcnt 15): wait for every vector memory operation in flight.
+constexpr unsigned kWaitVmemAll = 0x0F70;
+
 template <int K, int P>
 __device__ inline int poll_slots(const TrainArgs &a, const unsigned long long *slots, int base,
                                  unsigned tag, unsigned long long &m) {
@@ -380,6 +384,17 @@ __device__ inline int exchange_wait(const TrainArgs &a, int64_t e, unsigned long
                 }
             }
         }
+    } else if (G <= 256) {
+        // One group, and no loop around it (a loop head would make the
+        // compiler wait for every memory operation in flight).  Polling
+        // starts at once on small grids; beyond 16 workgroups it starts
+        // after this workgroup's key stores have completed, which measures
+        // faster there (the early polls only add traffic on the slot lines
+        // while the other workgroups' stores are still landing).
+        if (G > 16) __builtin_amdgcn_s_waitcnt(kWaitVmemAll);
+        abort = G <= 64    ? poll_slots<1, P>(a, slots, 0, tag, m)
+                : G <= 128 ? poll_slots<2, P>(a, slots, 0, tag, m)
+                           : poll_slots<4, P>(a, slots, 0, tag, m);
     } else {
         for (int base = 0; base < G && abort == 0; base += 256) {
             const int left = G - base;

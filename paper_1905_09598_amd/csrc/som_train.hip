@@ -181,7 +181,7 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
     // Polls in flight per exchange.  One-wave workgroups hold their sample
     // blocks across the exchange, and one poll at a time keeps those in
     // registers.
-    constexpr int kPolls = L == 64 ? 1 : 8;
+    constexpr int kPolls = L == 64 ? 1 : 4;
     const int lane = threadIdx.x & 63;
     const float inv_cols = 1.f / (float)a.cols;
     if (WPR > 1) {
@@ -513,9 +513,10 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
         if (a.variant >= 3) return hipErrorInvalidValue;
     }
     plan->grid = grid;
-    // measured: one slot per 128-byte line is fastest up to 64 workgroups,
-    // 32-byte spacing beyond
-    plan->slot_spread = grid <= 64 ? 16 : 4;
+    // Measured on MI355X.  One-poll exchanges (one-wave workgroups): one
+    // slot per 128-byte line is fastest up to 64 workgroups, 32-byte spacing
+    // beyond.  Multi-poll exchanges: packed slots (fewer lines per poll).
+    plan->slot_spread = in->lanes == 64 ? (grid <= 64 ? 16 : 4) : 1;
     plan->block = kTrainBlock;
     plan->variant = variant;
     plan->kslots = in->k;

@@ -107,7 +107,11 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                           (size_t)plan->lds_rows * P4 * 16;
         if (plan->lds_bytes < 84 * 1024) plan->lds_bytes = 84 * 1024;
         plan->block = 256;
-        plan->slot_spread = plan->grid <= 64 ? 16 : 4;
+        // Measured on MI355X: the LDS-resident kernels' multi-poll exchanges
+        // are fastest with packed slots, the streamed kernels' one-poll
+        // exchanges with one slot per 128-byte line up to 64 workgroups and
+        // 32-byte spacing beyond.
+        plan->slot_spread = plan->variant == 3 ? 1 : (plan->grid <= 64 ? 16 : 4);
         const PipeInstance *pi = pipe_for(plan->block_m, plan->kslots);
         PipeKernel fn = plan->variant == 3 ? pi->lds : pipe_stream_kernel(pi->m, pi->ks);
         int per_cu = 0;
