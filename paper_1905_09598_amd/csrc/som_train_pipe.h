@@ -323,12 +323,15 @@ struct SampleDots {
     static constexpr int N = dots_stride<M>();
     static constexpr int W = (N + 63) / 64;
     float v[W];
-    __device__ void load(const float *sdots, int64_t blk, int64_t nblocks) {
+    // Block blk < the number of blocks.  Lanes past the N entries load the
+    // last one again and are never read: no select on a loaded value, which
+    // would wait for the load right away.
+    __device__ void load(const float *sdots, int64_t blk) {
         const int lane = threadIdx.x & 63;
 #pragma unroll
         for (int w = 0; w < W; ++w) {
             const int t = 64 * w + lane;
-            v[w] = (t < N && blk < nblocks) ? sdots[blk * N + t] : 0.f;
+            v[w] = sdots[blk * N + (t < N ? t : N - 1)];
         }
     }
     __device__ float at(int t) const { return lane_f(v[t / 64], t % 64); }
@@ -384,17 +387,23 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
         for (int j = 0; j < M; ++j) gam_prev[j] = 0.f;
         const float4 p = lane < R ? l.pos[lane] : make_float4(0.f, 0.f, 0.f, 0.f);
         SampleDots<M> sd;
-        sd.load(a.block_dots, 0, nb);
+        sd.load(a.block_dots, 0);
+        // The sample products of the coming block, spread over the lanes in
+        // sd when loaded and read out into AA, AB, BB one block ahead: by the
+        // end of a block the loads have long landed (the block's exchange
+        // polls, issued after them, have been waited for), while reading them
+        // at the top of the block waited for every memory operation in flight.
+        float AA[T], AB[M * M], BB[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) AA[t] = sd.at(t);
+#pragma unroll
+        for (int t = 0; t < M * M; ++t) AB[t] = sd.at(T + t);
+#pragma unroll
+        for (int t = 0; t < T; ++t) BB[t] = AA[t];  // block 0: B = A
         __syncthreads();  // the sweepers' products of the initial prototypes
         for (int64_t blk = 0; blk < nb; ++blk) {
             const int par = (int)(blk & 1);
-            float AA[T], AB[M * M], BB[T], E[T], d[ND];
-#pragma unroll
-            for (int t = 0; t < T; ++t) AA[t] = sd.at(t);
-#pragma unroll
-            for (int t = 0; t < M * M; ++t) AB[t] = sd.at(T + t);
-#pragma unroll
-            for (int t = 0; t < T; ++t) BB[t] = blk == 0 ? AA[t] : sd.at(T + M * M + t);
+            float E[T], d[ND];
             const float *dr =
                 l.dots + ((size_t)(par ^ 1) * l.Rp + (lane < R ? lane : 0)) * kSweepers * ND;
 #pragma unroll
@@ -407,7 +416,7 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
                 for (int j = 1; j < M; ++j) d[M + j] = d[j];
             }
             gram_from_dots<M>(d, beta_prev, gam_prev, AA, AB, BB, E);
-            if (blk + 1 < nb) sd.load(a.block_dots, blk, nb);
+            if (blk + 1 < nb) sd.load(a.block_dots, blk);
             const int64_t s0 = blk * M;
             const int mb = (int)((a.nsteps - s0) < M ? (a.nsteps - s0) : M);
             float beta, gam[M];
@@ -421,6 +430,14 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
             beta_prev = beta;
 #pragma unroll
             for (int j = 0; j < M; ++j) gam_prev[j] = gam[j];
+            if (blk + 1 < nb) {
+#pragma unroll
+                for (int t = 0; t < T; ++t) AA[t] = sd.at(t);
+#pragma unroll
+                for (int t = 0; t < M * M; ++t) AB[t] = sd.at(T + t);
+#pragma unroll
+                for (int t = 0; t < T; ++t) BB[t] = sd.at(T + M * M + t);
+            }
             if (!ok && lane == 0) bc->abort = 1;
             __syncthreads();
             if (!ok) return;  // the sweepers read it from bc->abort

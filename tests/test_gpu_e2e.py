@@ -27,7 +27,8 @@ REL = 0.01
 
 @pytest.mark.parametrize("ci,topology", [(0, som.RECT), (1, som.RECT), (2, som.RECT),
                                          (3, som.RECT), (4, som.RECT),
-                                         (0, som.HEX), (1, som.HEX), (2, som.HEX)])
+                                         (0, som.HEX), (1, som.HEX), (2, som.HEX),
+                                         (3, som.HEX)])
 def test_full_training_matches_oracle_quality(ci, topology):
     cfg = config(ci)
     g = golden(cfg, hex_lattice=topology == som.HEX)
