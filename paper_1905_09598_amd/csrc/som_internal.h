@@ -50,6 +50,7 @@ struct TrainArgs {
     int32_t variant;        // requested variant: 0 any, 1 LDS-resident, 2 streamed
     int32_t lds_rows;       // pipelined streamed variant: leading rows of each
                             // workgroup kept in LDS (-1 = planner's choice)
+    int32_t block_m;        // pipelined kernel: requested block length (0 = any)
     uint64_t timeout_ticks; // bound of one exchange wait, in 100 MHz ticks
 };
 

@@ -23,11 +23,16 @@ constexpr PipeInstance pipe_instance() {
 
 // (M, KS): block length and float4 slices of 64 columns per sweeper (rows of
 // up to 3 * 64 * KS float4).  The sample registers, 3 M KS float4 per lane,
-// bound M * KS; with KS = 7 only the LDS variant stays out of scratch.  The
-// streamed kernels of the same shapes are listed in som_train_pipe_stream.hip.
-const PipeInstance kPipe[] = {pipe_instance<8, 1>(), pipe_instance<4, 1>(), pipe_instance<4, 2>(),
-                              pipe_instance<4, 3>(), pipe_instance<2, 3>(), pipe_instance<2, 4>(),
-                              pipe_instance<2, 7, false>()};
+// bound M * KS: the longer blocks (8 x 2, 6 x 3, 4 x 4) and KS = 7 stay out
+// of scratch only in the LDS variant, which has no streamed row registers.
+// The planner takes the cheapest shape for the row length; a longer block
+// spreads the per-block work of the controller over more steps.  The
+// streamed kernels are listed in som_train_pipe_stream.hip.
+const PipeInstance kPipe[] = {
+    pipe_instance<8, 1>(),        pipe_instance<4, 1>(),        pipe_instance<8, 2, false>(),
+    pipe_instance<4, 2>(),        pipe_instance<6, 3, false>(), pipe_instance<4, 3>(),
+    pipe_instance<2, 3>(),        pipe_instance<4, 4, false>(), pipe_instance<2, 4>(),
+    pipe_instance<2, 7, false>()};
 
 const PipeInstance *pipe_for(int m, int ks) {
     for (const PipeInstance &p : kPipe)
@@ -55,7 +60,7 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
     const int max_grid = a.N < num_cus ? a.N : num_cus;
     double best = 1e300;
     for (const PipeInstance &pi : kPipe) {
-        if (pi.ks != ks_need) continue;
+        if (pi.ks != ks_need || (a.block_m > 0 && pi.m != a.block_m)) continue;
         for (int v = 0; v < 2; ++v) {
             const bool ldsw = v == 0;  // LDS first: it wins ties
             if ((a.variant == 1 && !ldsw) || (a.variant == 2 && ldsw)) continue;

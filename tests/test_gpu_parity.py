@@ -430,6 +430,27 @@ def test_training_shapes_follow_the_oracle(rows, cols, d, n, epochs, variant, mo
         assert plan["variant"] in (0, 1)
 
 
+# Every block length the pipelined kernel is built with, forced through
+# SOM_TRAIN_BLOCK_M on a row length of its float4-slice count KS (row pitch
+# 256 / 512, 1024, 2048, 3072 and 5120 floats: d up to 512, 1024, 2048,
+# 3072 and 5120).  The LDS-resident variant runs every one of them.
+@pytest.mark.parametrize("rows,cols,d,n,epochs,block_m", [
+    (7, 9, 64, 101, 2, 8), (7, 9, 64, 101, 2, 4),            # KS = 1
+    (12, 12, 777, 83, 2, 8), (12, 12, 777, 83, 2, 4),        # KS = 2
+    (20, 13, 1500, 61, 2, 6), (9, 50, 2048, 40, 1, 6),       # KS = 3
+    (20, 13, 1500, 61, 2, 4), (20, 13, 1500, 61, 2, 2),
+    (6, 5, 3000, 30, 2, 4), (6, 5, 3000, 30, 2, 2),          # KS = 4
+    (5, 4, 5000, 30, 1, 2),                                  # KS = 7
+])
+def test_pipelined_block_lengths_follow_the_oracle(rows, cols, d, n, epochs, block_m,
+                                                   monkeypatch):
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", "3")
+    monkeypatch.setenv("SOM_TRAIN_BLOCK_M", str(block_m))
+    say("pipelined block length", block_m, "shape", rows, cols, d, n, epochs)
+    plan = _train_vs_oracle(rows, cols, d, n, epochs)
+    assert plan["variant"] == 3
+
+
 @pytest.mark.parametrize("lds_rows", ["0", "1", "7", "64"])
 @pytest.mark.parametrize("rows,cols,d,n,epochs", [(20, 13, 1500, 61, 2), (11, 12, 2048, 40, 1)])
 def test_streamed_variant_with_leading_rows_in_lds(rows, cols, d, n, epochs, lds_rows,
