@@ -21,6 +21,7 @@ stream, against the 8 TB/s HBM peak.
 the same training run.
 """
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -61,12 +62,13 @@ def measured_traffic(workload: str):
     return ent.get("bytes_per_launch")
 
 
-def cpu_baseline(cfg, X, order, budget_s: float):
-    """fp64 oracle on the host over a prefix of the same training run."""
+def cpu_baseline(cfg, X, order, budget_s: float, threads: int = 0):
+    """fp64 oracle on the host over a prefix of the same training run, on
+    `threads` OpenMP threads (0: every core this process may use)."""
     import numpy as np
     import oracle
 
-    threads = oracle.default_threads()
+    threads = threads or oracle.default_threads()
     W = oracle.init_uniform(cfg.init_seed, cfg.units, cfg.d)
     s = oracle.schedule(cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1,
                         oracle.LINEAR, oracle.EXPONENTIAL)
@@ -87,6 +89,36 @@ def cpu_baseline(cfg, X, order, budget_s: float):
         "sample": f"first {done} of {cfg.steps} training steps of {cfg.name} "
                   f"(fp64, {threads} OpenMP threads, {dt:.1f} s)",
     }
+
+
+def stream_reference(nbytes: int, reps: int = 5) -> dict:
+    """Same-footprint memory reference: c = a + b over three fp32 buffers of
+    nbytes each (two reads and one write per element, the access pattern of
+    the algorithmic 3 N d 4 bytes), best of reps, timed with HIP events on
+    the current stream.  Plain torch arithmetic: a bandwidth reference for
+    the roofline, not part of the SOM path."""
+    import torch
+
+    n = max(1, nbytes // 4)
+    a = torch.ones(n, dtype=torch.float32, device="cuda")
+    b = torch.ones(n, dtype=torch.float32, device="cuda")
+    c = torch.empty_like(a)
+    torch.add(a, b, out=c)
+    best, inner = None, 20
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(inner):
+            torch.add(a, b, out=c)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / inner
+        best = ms if best is None else min(best, ms)
+    return {"bytes": 3 * n * 4, "ms": best, "GB/s": 3 * n * 4 / (best / 1e3) / 1e9,
+            "what": f"c = a + b over three buffers the size of W (torch), {inner} launches "
+                    f"back to back, best of {reps}: the bandwidth a plain stream of the "
+                    "same footprint reaches, launch gaps included (L2 / MALL resident "
+                    "when W fits)"}
 
 
 def map_sweep(cpu_budget: float):
@@ -194,6 +226,12 @@ def main():
     ap.add_argument("--input", choices=("dense", "csr"), default="dense",
                     help="train from the dense rows (som_train) or from their CSR form "
                          "(som_train_csr, the sparse-input path)")
+    ap.add_argument("--shard", type=int, default=1, metavar="G",
+                    help="train one GPU's share of the workload's map when its prototype "
+                         "rows are split over G GPUs: N / G units (as near-square a map as "
+                         "divides N / G), the same samples, d and schedule; the arg-min "
+                         "exchange between GPUs is not built, so this is the per-GPU "
+                         "kernel at its real shape")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (the "
                          "reference dispatch for scaling HBM byte counters) and exit")
@@ -226,6 +264,19 @@ def main():
     import workloads
 
     cfg = workloads.WORKLOADS[args.workload]
+    shard = None
+    if args.shard > 1:
+        base = cfg
+        if base.units % args.shard:
+            sys.exit(f"bench.py: --shard {args.shard} does not divide the {base.units} units")
+        share = base.units // args.shard
+        r = max(k for k in range(1, int(share ** 0.5) + 1) if share % k == 0)
+        cfg = dataclasses.replace(base, name=f"{base.name}_shard{args.shard}", rows=r,
+                                  cols=share // r)
+        shard = {"of_workload": base.name, "gpus": args.shard, "units": share,
+                 "map": f"{r}x{share // r}",
+                 "note": "one GPU's share of the prototype rows, same samples, d and schedule; "
+                         "the per-step arg-min exchange between GPUs is not built"}
     X = workloads.make_data(cfg)
     order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)
     torch.cuda.set_device(0)
@@ -352,12 +403,18 @@ def main():
         "qe": qe,
         "te": te,
     }
+    if shard:
+        out["config"]["shard"] = shard
     if sparse:
         out["roofline"]["note"] = ("sparse path: bytes = the samples' non-zeros gathered and "
                                    "scattered in fp64 for every unit; its step is bound by the "
                                    "grid exchange's latency, not by bytes")
+    out["stream_reference"] = stream_reference(cfg.units * cfg.d * 4)
     if args.cpu_budget > 0:
         out["cpu_baseline"] = cpu_baseline(cfg, X, order, args.cpu_budget)
+        # the same oracle on one core (a third of the budget), for the
+        # single-core speed-up
+        out["cpu_baseline_1core"] = cpu_baseline(cfg, X, order, args.cpu_budget / 3, threads=1)
     print(json.dumps(out), flush=True)
     m.close()
 
