@@ -249,14 +249,19 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
                 }
                 issue(r + D, ring[u], cring[u]);
                 if (DOTS) {
-                    wave_sums_last<NA>(acc);
-                    if (lane == 63) {
+                    constexpr int NT = (NA + 3) / 4;
+                    float tot[NT];
+                    wave_sums_rows<NA>(acc, tot);
+                    const float fz = lane_f(tot[ND / 4], 16 * sum_row(ND));
+                    if ((lane & 15) == 0) {
+                        // lane 16 q writes the values its row holds
                         float *dr = dots + (r * kSweepers + s) * ND;
-                        dr[0] = acc[0];
+                        const int q = lane >> 4;
 #pragma unroll
-                        for (int t = 1; t < ND; ++t) {
-                            const bool used = t < M ? ADOT : BDOT;
-                            dr[t] = used ? acc[t] - acc[ND] : 0.f;
+                        for (int j = 0; j < NT; ++j) {
+                            const int t = 4 * j + 2 * (q & 1) + (q >> 1);  // sum_row(t) == q
+                            const bool used = t == 0 || (t < M ? ADOT : BDOT);
+                            if (t < ND) dr[t] = t == 0 ? tot[j] : (used ? tot[j] - fz : 0.f);
                         }
                     }
                 }
