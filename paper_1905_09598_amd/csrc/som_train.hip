@@ -141,12 +141,19 @@ __device__ inline void sweep(f4 *rows_p, int R, const f4 (&xu)[M][K], const f4 (
                 }
             }
             if (GRAM) {
-                wave_sums<T>(acc);
-                if (lane == 0) {
+                constexpr int NT = (T + 3) / 4;
+                float tot[NT];
+                wave_sums_rows<T>(acc, tot);
+                if ((lane & 15) == 0) {
+                    // lane 16 q writes the sums its row holds
+                    const int q = lane >> 4;
 #pragma unroll
-                    for (int t = 0; t < T; ++t) {
-                        if (WPR == 1) E[r * T + t] = acc[t];
-                        else part[(r * T + t) * WPR + wig] = acc[t];
+                    for (int j = 0; j < NT; ++j) {
+                        const int t = 4 * j + 2 * (q & 1) + (q >> 1);  // sum_row(t) == q
+                        if (t < T) {
+                            if (WPR == 1) E[r * T + t] = tot[j];
+                            else part[(r * T + t) * WPR + wig] = tot[j];
+                        }
                     }
                 }
             }
