@@ -331,9 +331,9 @@ using Pos = std::integral_constant<int, q>;
 // (expcnt 7, lgkmcnt 15): wait for every vector memory operation in flight.
 constexpr unsigned kWaitVmemAll = 0x0F70;
 
-template <int K, int P>
-__device__ inline int poll_slots(const TrainArgs &a, const unsigned long long *slots, int base,
-                                 unsigned tag, unsigned long long &m) {
+template <int K, int P, typename Work>
+__device__ __forceinline__ int poll_slots(const TrainArgs &a, const unsigned long long *slots, int base,
+                                 unsigned tag, unsigned long long &m, Work &&work) {
     static_assert(P == 4 || P == 8, "four or eight polls in flight");
     const int lane = threadIdx.x & 63, G = a.grid, sp = a.slot_spread;
     const unsigned long long *adr[K];
@@ -349,6 +349,7 @@ __device__ inline int poll_slots(const TrainArgs &a, const unsigned long long *s
 #pragma unroll
     for (int q = 0; q < P; ++q)
         v[q] = __hip_atomic_load(adr[q % K], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    work();  // the caller's work, while the first polls are in flight
     // Check position q and put its next poll in flight (before the exit
     // test: a poll skipped on the way out would leave the loop head unsure
     // which load is the oldest); true once no lane misses a key.
@@ -393,22 +394,29 @@ __device__ inline int poll_slots(const TrainArgs &a, const unsigned long long *s
 
 // Wait for every workgroup's key of exchange e and return the winning unit
 // (the same in all lanes), or -1 if the wait was given up.  `best` is this
-// workgroup's own key (the answer when the grid is one workgroup).  P polls
+// workgroup's own key (the answer when the grid is one workgroup).  `work`
+// (independent of the result) runs once, while the wait is under way.  P polls
 // per lane are kept in flight: 4 or 8, or 1 (each lane waits for its slots
 // one after the other: the fewest registers and the least polling traffic).
-template <int P>
-__device__ inline int exchange_wait(const TrainArgs &a, int64_t e, unsigned long long best) {
+template <int P, typename Work>
+__device__ __forceinline__ int exchange_wait(const TrainArgs &a, int64_t e, unsigned long long best,
+                                    Work &&work) {
     const int lane = threadIdx.x & 63, G = a.grid;
-    if (G == 1) return (int)(best & (unsigned long long)kMaxUnits);
+    if (G == 1) {
+        work();
+        return (int)(best & (unsigned long long)kMaxUnits);
+    }
     const unsigned tag = 0x80u | (unsigned)((e >> 1) & 0x7f);
     const int64_t par = (e & 1) * (int64_t)G * a.slot_spread;
     const unsigned long long *slots =
         a.slots + (blockIdx.x % kSlotReplicas) * kSlotReplicaStride + par;
     unsigned long long m = ~0ull;
     int abort = 0;
+    const auto none = [] {};
     if constexpr (P == 1) {
         // One poll per lane at a time, each lane waiting for its slots one
         // after the other: the fewest registers.
+        work();
         const int sp = a.slot_spread;
         for (int i = lane; i < G && abort == 0; i += 64) {
             const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
@@ -439,17 +447,22 @@ __device__ inline int exchange_wait(const TrainArgs &a, int64_t e, unsigned long
         // after this workgroup's key stores have completed, which measures
         // faster there (the early polls only add traffic on the slot lines
         // while the other workgroups' stores are still landing).
-        if (G > 16) __builtin_amdgcn_s_waitcnt(kWaitVmemAll);
-        abort = G <= 64    ? poll_slots<1, P>(a, slots, 0, tag, m)
-                : G <= 128 ? poll_slots<2, P>(a, slots, 0, tag, m)
-                           : poll_slots<4, P>(a, slots, 0, tag, m);
-    } else {
-        for (int base = 0; base < G && abort == 0; base += 256) {
-            const int left = G - base;
-            abort = left <= 64    ? poll_slots<1, P>(a, slots, base, tag, m)
-                    : left <= 128 ? poll_slots<2, P>(a, slots, base, tag, m)
-                                  : poll_slots<4, P>(a, slots, base, tag, m);
+        // The caller's work runs while the key stores complete, or on small
+        // grids while the first polls are in flight.
+        if (G > 16) {
+            work();
+            __builtin_amdgcn_s_waitcnt(kWaitVmemAll);
+            abort = G <= 64    ? poll_slots<1, P>(a, slots, 0, tag, m, none)
+                    : G <= 128 ? poll_slots<2, P>(a, slots, 0, tag, m, none)
+                               : poll_slots<4, P>(a, slots, 0, tag, m, none);
+        } else {
+            abort = poll_slots<1, P>(a, slots, 0, tag, m, work);
         }
+    } else {
+        // groups of 256 (slots past the grid count as received)
+        work();
+        for (int base = 0; base < G && abort == 0; base += 256)
+            abort = poll_slots<4, P>(a, slots, base, tag, m, none);
     }
     // The timeout is recorded after the polls: a store among them would mix
     // stores into the loads in flight, and the compiler then waits for every
@@ -472,7 +485,7 @@ __device__ inline int exchange_wait(const TrainArgs &a, int64_t e, unsigned long
 template <int P>
 __device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long best) {
     exchange_publish(a, e, best);
-    return exchange_wait<P>(a, e, best);
+    return exchange_wait<P>(a, e, best, [] {});
 }
 
 // Neighbourhood factor of owned row r given BMU c: lr * 2^(-g * c2) with g
@@ -519,17 +532,34 @@ __device__ inline bool block_steps(const TrainArgs &a, int64_t s0, int mb, int r
         gam[j] = 0.f;
         lin[j] = 0.f;
     }
+    if (mb <= 0) return true;
+    const auto key_of = [&](float D) {
+        return wave_argmin_key(lane < R ? dist_order_bits(D) : 0xffffffffu, r0);
+    };
+    // Each step publishes the next step's key as soon as its distance is
+    // known (it needs only quad and lin_{k+1}); the rest of its bookkeeping
+    // runs inside the next exchange's wait, off the path from one exchange
+    // to the next.  Step 0's distance is E_00 (no step taken yet).
+    const auto book = [&](int k, float h, float om) {
+#pragma unroll
+        for (int l = k + 2; l < M; ++l) lin[l] = fmaf(h, E[tri(k, l)], om * lin[l]);
+        beta *= om;
+#pragma unroll
+        for (int j = 0; j < k; ++j) gam[j] *= om;
+        gam[k] = h;
+    };
+    float2 sc = sw.get(a, s0);
+    unsigned long long best = key_of(E[tri(0, 0)]);
+    exchange_publish(a, s0, best);
     bool ok = true;
+    float h_prev = 0.f, om_prev = 1.f;
 #pragma unroll
     for (int k = 0; k < M; ++k) {
         if (k >= mb || !ok) continue;
         const int64_t s = s0 + k;
-        const float2 sc = sw.get(a, s);
-        const float Ekk = E[tri(k, k)];
-        const float D = fmaf(-2.f, lin[k], Ekk) + quad;
-        const unsigned long long best =
-            wave_argmin_key(lane < R ? dist_order_bits(D) : 0xffffffffu, r0);
-        const int c = exchange<P>(a, s, best);
+        const int c = exchange_wait<P>(a, s, best, [&] {
+            if (k > 0) book(k - 1, h_prev, om_prev);
+        });
         if (c < 0) {
             ok = false;
             continue;
@@ -538,13 +568,17 @@ __device__ inline bool block_steps(const TrainArgs &a, int64_t s0, int mb, int r
         unit_rc(c, a.cols, inv_cols, cr, cc);
         const float h = neighbour_h(a, p, (float)cr, (float)cc, (float)(cr & 1), sc.x, sc.y);
         const float om = 1.f - h;
-        quad = fmaf(om * om, quad, h * fmaf(2.f * om, lin[k], h * Ekk));
-#pragma unroll
-        for (int l = k + 1; l < M; ++l) lin[l] = fmaf(h, E[tri(k, l)], om * lin[l]);
-        beta *= om;
-#pragma unroll
-        for (int j = 0; j < k; ++j) gam[j] *= om;
-        gam[k] = h;
+        quad = fmaf(om * om, quad, h * fmaf(2.f * om, lin[k], h * E[tri(k, k)]));
+        if (k + 1 < M) lin[k + 1] = fmaf(h, E[tri(k, k + 1)], om * lin[k + 1]);
+        if (k + 1 < mb) {
+            sc = sw.get(a, s + 1);
+            best = key_of(fmaf(-2.f, lin[k + 1], E[tri(k + 1, k + 1)]) + quad);
+            exchange_publish(a, s + 1, best);
+            h_prev = h;
+            om_prev = om;
+        } else {
+            book(k, h, om);  // the block's last step: no wait follows
+        }
         if (blockIdx.x == 0 && lane == 0 && a.bmu_trace) a.bmu_trace[s] = c;
     }
     return ok;

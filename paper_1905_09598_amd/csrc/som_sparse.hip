@@ -445,7 +445,7 @@ __device__ inline void sparse_exchange_wave(const TrainArgs &a, int *bmu, int *a
     const int lane = threadIdx.x & 63;
     for (int64_t s = 0; s < nsteps4; ++s) {
         if (a.grid > 1) {
-            const int c = exchange_wait<1>(a, s, 0ull);
+            const int c = exchange_wait<1>(a, s, 0ull, [] {});
             if (lane == 0) {
                 if (c < 0)
                     *abort = 1;
