@@ -327,13 +327,28 @@ __device__ inline void exchange_publish(const TrainArgs &a, int64_t e, unsigned 
 template <int q>
 using Pos = std::integral_constant<int, q>;
 
+// The registers an exchange polls into, kept by the caller from one
+// exchange to the next.  An exchange returns with polls still in flight;
+// were their registers free, the compiler would reuse them at once and wait
+// for those polls first (a memory round trip for the newest).  Held by the
+// caller, they stay untouched until the next exchange, which lets them land
+// (a load into a register whose previous load is still in flight needs no
+// wait) and marks them used only where they have landed anyway.
+template <int P>
+struct PollRegs {
+    unsigned long long v[P];
+};
+template <>
+struct PollRegs<1> {};
+
 // s_waitcnt immediate for vmcnt(0) with the other counters left alone
 // (expcnt 7, lgkmcnt 15): wait for every vector memory operation in flight.
 constexpr unsigned kWaitVmemAll = 0x0F70;
 
 template <int K, int P, typename Work>
-__device__ __forceinline__ int poll_slots(const TrainArgs &a, const unsigned long long *slots, int base,
-                                 unsigned tag, unsigned long long &m, Work &&work) {
+__device__ __forceinline__ int poll_slots(const TrainArgs &a, const unsigned long long *slots,
+                                          int base, unsigned tag, unsigned long long &m,
+                                          Work &&work, PollRegs<P> &pr) {
     static_assert(P == 4 || P == 8, "four or eight polls in flight");
     const int lane = threadIdx.x & 63, G = a.grid, sp = a.slot_spread;
     const unsigned long long *adr[K];
@@ -345,7 +360,7 @@ __device__ __forceinline__ int poll_slots(const TrainArgs &a, const unsigned lon
         adr[k] = slots + (int64_t)(mine ? i : base) * sp;
         need |= mine ? 1u << k : 0u;
     }
-    unsigned long long v[P];
+    unsigned long long(&v)[P] = pr.v;  // the caller's registers
 #pragma unroll
     for (int q = 0; q < P; ++q)
         v[q] = __hip_atomic_load(adr[q % K], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -399,8 +414,9 @@ __device__ __forceinline__ int poll_slots(const TrainArgs &a, const unsigned lon
 // per lane are kept in flight: 4 or 8, or 1 (each lane waits for its slots
 // one after the other: the fewest registers and the least polling traffic).
 template <int P, typename Work>
-__device__ __forceinline__ int exchange_wait(const TrainArgs &a, int64_t e, unsigned long long best,
-                                    Work &&work) {
+__device__ __forceinline__ int exchange_wait(const TrainArgs &a, int64_t e,
+                                             unsigned long long best, Work &&work,
+                                             PollRegs<P> &pr) {
     const int lane = threadIdx.x & 63, G = a.grid;
     if (G == 1) {
         work();
@@ -452,17 +468,27 @@ __device__ __forceinline__ int exchange_wait(const TrainArgs &a, int64_t e, unsi
         if (G > 16) {
             work();
             __builtin_amdgcn_s_waitcnt(kWaitVmemAll);
-            abort = G <= 64    ? poll_slots<1, P>(a, slots, 0, tag, m, none)
-                    : G <= 128 ? poll_slots<2, P>(a, slots, 0, tag, m, none)
-                               : poll_slots<4, P>(a, slots, 0, tag, m, none);
+            // the previous exchange's polls have landed with everything else
+#pragma unroll
+            for (int q = 0; q < P; ++q) asm volatile("" ::"v"(pr.v[q]));
+            abort = G <= 64    ? poll_slots<1, P>(a, slots, 0, tag, m, none, pr)
+                    : G <= 128 ? poll_slots<2, P>(a, slots, 0, tag, m, none, pr)
+                               : poll_slots<4, P>(a, slots, 0, tag, m, none, pr);
         } else {
-            abort = poll_slots<1, P>(a, slots, 0, tag, m, work);
+            // Small grids poll at once: a use of the previous exchange's
+            // poll registers waits only for those of its polls still in
+            // flight, which have had a step's work to land.
+#pragma unroll
+            for (int q = 0; q < P; ++q) asm volatile("" ::"v"(pr.v[q]));
+            abort = poll_slots<1, P>(a, slots, 0, tag, m, work, pr);
         }
     } else {
         // groups of 256 (slots past the grid count as received)
         work();
+#pragma unroll
+        for (int q = 0; q < P; ++q) asm volatile("" ::"v"(pr.v[q]));
         for (int base = 0; base < G && abort == 0; base += 256)
-            abort = poll_slots<4, P>(a, slots, base, tag, m, none);
+            abort = poll_slots<4, P>(a, slots, base, tag, m, none, pr);
     }
     // The timeout is recorded after the polls: a store among them would mix
     // stores into the loads in flight, and the compiler then waits for every
@@ -483,9 +509,10 @@ __device__ __forceinline__ int exchange_wait(const TrainArgs &a, int64_t e, unsi
 // array and polls the copy of its own XCD; slots alternate by the parity
 // of e and carry a tag of e, so a slot is never read for the wrong step.
 template <int P>
-__device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long best) {
+__device__ inline int exchange(const TrainArgs &a, int64_t e, unsigned long long best,
+                               PollRegs<P> &pr) {
     exchange_publish(a, e, best);
-    return exchange_wait<P>(a, e, best, [] {});
+    return exchange_wait<P>(a, e, best, [] {}, pr);
 }
 
 // Neighbourhood factor of owned row r given BMU c: lr * 2^(-g * c2) with g
@@ -519,11 +546,12 @@ __device__ inline float neighbour_h(const TrainArgs &a, float4 p, float cr, floa
 //   quad <- (1 - h)^2 quad + 2 h (1 - h) lin_k + h^2 E_kk,
 //   lin_l <- (1 - h) lin_l + h E_kl.
 // Returns false if an exchange was given up.  P: polls in flight per lane
-// in each exchange.
+// in each exchange, into the caller's registers pr.
 template <int M, int P>
 __device__ inline bool block_steps(const TrainArgs &a, int64_t s0, int mb, int r0, int R,
                                    const float (&E)[M * (M + 1) / 2], float4 p, float inv_cols,
-                                   StepWindow<float2> &sw, float &beta, float (&gam)[M]) {
+                                   StepWindow<float2> &sw, float &beta, float (&gam)[M],
+                                   PollRegs<P> &pr) {
     const int lane = threadIdx.x & 63;
     float lin[M], quad = 0.f;
     beta = 1.f;
@@ -557,9 +585,12 @@ __device__ inline bool block_steps(const TrainArgs &a, int64_t s0, int mb, int r
     for (int k = 0; k < M; ++k) {
         if (k >= mb || !ok) continue;
         const int64_t s = s0 + k;
-        const int c = exchange_wait<P>(a, s, best, [&] {
-            if (k > 0) book(k - 1, h_prev, om_prev);
-        });
+        const int c = exchange_wait<P>(
+            a, s, best,
+            [&] {
+                if (k > 0) book(k - 1, h_prev, om_prev);
+            },
+            pr);
         if (c < 0) {
             ok = false;
             continue;

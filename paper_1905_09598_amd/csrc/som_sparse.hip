@@ -443,9 +443,10 @@ struct SparseLane {
 __device__ inline void sparse_exchange_wave(const TrainArgs &a, int *bmu, int *abort,
                                             int64_t nsteps4) {
     const int lane = threadIdx.x & 63;
+    PollRegs<1> no_regs;  // one poll at a time: none left in flight
     for (int64_t s = 0; s < nsteps4; ++s) {
         if (a.grid > 1) {
-            const int c = exchange_wait<1>(a, s, 0ull, [] {});
+            const int c = exchange_wait<1>(a, s, 0ull, [] {}, no_regs);
             if (lane == 0) {
                 if (c < 0)
                     *abort = 1;

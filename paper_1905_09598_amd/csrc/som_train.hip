@@ -189,6 +189,7 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
     // blocks across the exchange, and one poll at a time keeps those in
     // registers.
     constexpr int kPolls = L == 64 ? 1 : 4;
+    PollRegs<kPolls> pr{};  // exchange poll registers, held between this block's exchanges
     const int lane = threadIdx.x & 63;
     const float inv_cols = 1.f / (float)a.cols;
     if (WPR > 1) {
@@ -206,7 +207,7 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
 #pragma unroll
         for (int t = 0; t < T; ++t) Er[t] = lane < R ? E[lane * T + t] : 0.f;
         if (lane < R) p = pos[lane];
-        const bool ok = block_steps<M, kPolls>(a, s0, mb, r0, R, Er, p, inv_cols, sw, beta, gam);
+        const bool ok = block_steps<M, kPolls>(a, s0, mb, r0, R, Er, p, inv_cols, sw, beta, gam, pr);
         if (lane < R) {
             coef[lane * (M + 1)] = beta;
 #pragma unroll
@@ -240,7 +241,7 @@ __device__ inline bool block_bmus(const TrainArgs &a, int64_t s0, int mb, int r0
             best = u64_min(best, row_key(D, r0 + r));
         }
         best = wave_min_key(best, false);
-        const int c = exchange<kPolls>(a, s, best);
+        const int c = exchange<kPolls>(a, s, best, pr);
         if (c < 0) return false;
         if (blockIdx.x == 0 && lane == 0 && a.bmu_trace) a.bmu_trace[s] = c;
         const float2 sc = sw.get(a, s);

@@ -393,6 +393,7 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
         const float4 p = lane < R ? l.pos[lane] : make_float4(0.f, 0.f, 0.f, 0.f);
         SampleDots<M> sd;
         sd.load(a.block_dots, 0);
+        PollRegs<kPolls> pr{};  // exchange poll registers, held across blocks
         // The sample products of the coming block, spread over the lanes in
         // sd when loaded and read out into AA, AB, BB one block ahead: by the
         // end of a block the loads have long landed (the block's exchange
@@ -425,7 +426,7 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
             const int64_t s0 = blk * M;
             const int mb = (int)((a.nsteps - s0) < M ? (a.nsteps - s0) : M);
             float beta, gam[M];
-            const bool ok = block_steps<M, kPolls>(a, s0, mb, r0, R, E, p, inv_cols, sw, beta, gam);
+            const bool ok = block_steps<M, kPolls>(a, s0, mb, r0, R, E, p, inv_cols, sw, beta, gam, pr);
             if (lane < R) {
                 float *cf = l.coef + ((size_t)par * l.Rp + lane) * (M + 1);
                 cf[0] = beta;
