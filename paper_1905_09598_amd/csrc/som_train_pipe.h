@@ -184,16 +184,17 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
     const int lane = threadIdx.x & 63, s = threadIdx.x >> 6;
     f4 ring[D][KS];
     float cring[D][M + 1];
-    // Loads are unconditional (clamped row and column, unused or zeroed
-    // when out of range) so that a burst of them is waited for once.
+    // Loads are unconditional (clamped row and column, unused when out of
+    // range) so that a burst of them is waited for once.  Slices past the
+    // sweeper's share are zeroed where they are used, not here: a select on
+    // a value as it is loaded makes the compiler wait for the load on the
+    // spot, which would cancel the rows' prefetch.
     auto issue = [&](int r, f4 (&dst)[KS], float (&cdst)[M + 1]) {
         const int rr = r < R ? r : R - 1;
 #pragma unroll
         for (int t = 0; t < KS; ++t) {
             const int q = 64 * (s + kSweepers * t) + lane;
-            const f4 v = rows[(size_t)rr * P4 + (q < P4 ? q : P4 - 1)];
-            const f4 zero = {0.f, 0.f, 0.f, 0.f};
-            dst[t] = t < nw ? v : zero;
+            dst[t] = rows[(size_t)rr * P4 + (q < P4 ? q : P4 - 1)];
         }
         if (MAT) {
 #pragma unroll
@@ -214,7 +215,8 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
 #pragma unroll
                 for (int t = 0; t < KS; ++t) {
                     {
-                        f4 w = ring[u][t];
+                        const f4 zero = {0.f, 0.f, 0.f, 0.f};
+                        f4 w = t < nw ? ring[u][t] : zero;
                         if (MAT) {
                             w = w * cring[u][0];
 #pragma unroll
