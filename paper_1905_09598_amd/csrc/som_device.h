@@ -12,6 +12,7 @@ namespace som {
 namespace dev {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int32_t kStatusTimeout = 5;  // SOM_E_TIMEOUT
 

@@ -180,21 +180,37 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
     constexpr int ND = 2 * M;
     constexpr bool DOTS = ADOT || BDOT;
     constexpr int NA = ND + 1;  // f.f, f.x_i, f.xn_j and f.z (last)
-    row_t<LDSW> *rows = rows_as<LDSW>(rows_p);
+    [[maybe_unused]] row_t<LDSW> *rows = rows_as<LDSW>(rows_p);
     const int lane = threadIdx.x & 63, s = threadIdx.x >> 6;
+    // Streamed rows go through a buffer resource over the R rows: a slice
+    // past the sweeper's share gets an offset beyond its end, so that its
+    // load returns zeros and its store is dropped, with no select or branch
+    // (either would make the compiler wait for the row loads in flight).
+    // (unused by the LDS variant)
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(rows_p, (short)0, LDSW ? 0 : R * P4 * 16, 0x00020000);
+    constexpr int kOutside = 1 << 30;  // bytes, beyond any sweep's rows
+    const auto slice_off = [&](int r, int t) {
+        return t < nw ? (r * P4 + 64 * (s + kSweepers * t) + lane) * 16 : kOutside;
+    };
     f4 ring[D][KS];
     float cring[D][M + 1];
     // Loads are unconditional (clamped row and column, unused when out of
-    // range) so that a burst of them is waited for once.  Slices past the
-    // sweeper's share are zeroed where they are used, not here: a select on
-    // a value as it is loaded makes the compiler wait for the load on the
+    // range) so that a burst of them is waited for once.  In LDS, slices past
+    // the sweeper's share are zeroed where they are used, not here: a select
+    // on a value as it is loaded makes the compiler wait for the load on the
     // spot, which would cancel the rows' prefetch.
     auto issue = [&](int r, f4 (&dst)[KS], float (&cdst)[M + 1]) {
         const int rr = r < R ? r : R - 1;
 #pragma unroll
         for (int t = 0; t < KS; ++t) {
-            const int q = 64 * (s + kSweepers * t) + lane;
-            dst[t] = rows[(size_t)rr * P4 + (q < P4 ? q : P4 - 1)];
+            if constexpr (LDSW) {
+                const int q = 64 * (s + kSweepers * t) + lane;
+                dst[t] = rows[(size_t)rr * P4 + (q < P4 ? q : P4 - 1)];
+            } else {
+                dst[t] = __builtin_bit_cast(
+                    f4, __builtin_amdgcn_raw_buffer_load_b128(rs, slice_off(rr, t), 0, 0));
+            }
         }
         if (MAT) {
 #pragma unroll
@@ -216,7 +232,7 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
                 for (int t = 0; t < KS; ++t) {
                     {
                         const f4 zero = {0.f, 0.f, 0.f, 0.f};
-                        f4 w = t < nw ? ring[u][t] : zero;
+                        f4 w = (!LDSW || t < nw) ? ring[u][t] : zero;
                         if (MAT) {
                             w = w * cring[u][0];
 #pragma unroll
@@ -227,7 +243,12 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
                                 w.z = fmaf(g, xp[i][t].z, w.z);
                                 w.w = fmaf(g, xp[i][t].w, w.w);
                             }
-                            if (t < nw) rows[(size_t)r * P4 + 64 * (s + kSweepers * t) + lane] = w;
+                            if constexpr (LDSW) {
+                                if (t < nw) rows[(size_t)r * P4 + 64 * (s + kSweepers * t) + lane] = w;
+                            } else {
+                                __builtin_amdgcn_raw_buffer_store_b128(
+                                    __builtin_bit_cast(u32x4, w), rs, slice_off(r, t), 0, 0);
+                            }
                         }
                         if (DOTS) {
                             // f.(x - z) as f.x - f.z after the lane sums:
