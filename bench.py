@@ -379,6 +379,7 @@ def main():
             "train_steps_per_pass": cfg.steps,
             "schedule": f"lr {cfg.lr0}->{cfg.lr1} linear, sigma {cfg.sigma0}->{cfg.sigma1} exp",
             "grid": grid, "block": block, "variant": variant, "input": args.input,
+            "block_steps": None if sparse else plan["block_steps"],
         },
         "roofline": {
             "bound": "hbm",

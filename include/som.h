@@ -270,12 +270,13 @@ som_status som_suggest_size(int64_t m, double lambda1, double lambda2, int32_t *
 som_status som_init_linear(som_map *map, const float *X, int64_t n);
 
 /* Launch shape that som_train would use for this map: workgroups, threads
- * per workgroup and kernel variant (0 = prototypes streamed from memory once
+ * per workgroup, kernel variant (0 = prototypes streamed from memory once
  * per block of steps, 1 = prototypes held in LDS for the whole call, 2 / 3 =
  * the same with the pass over the prototypes overlapped with the grid
- * exchanges).  Any output may be NULL. */
+ * exchanges) and steps per block (the number of consecutive samples whose
+ * updates one pass over the prototypes applies).  Any output may be NULL. */
 som_status som_train_plan(const som_map *map, int32_t *grid, int32_t *block,
-                          int32_t *variant);
+                          int32_t *variant, int32_t *block_steps);
 
 /* Human-readable name of a status code (static storage). */
 const char *som_status_string(som_status status);

@@ -108,7 +108,7 @@ def lib():
         "som_get_shape": [vp, C.POINTER(i32), C.POINTER(i32), C.POINTER(i32),
                           C.POINTER(i32)],
         "som_shuffle": [u64, i64, i64, vp],
-        "som_train_plan": [vp, C.POINTER(i32), C.POINTER(i32), C.POINTER(i32)],
+        "som_train_plan": [vp, C.POINTER(i32), C.POINTER(i32), C.POINTER(i32), C.POINTER(i32)],
         "som_pca2": [vp, i64, i32, vp, C.POINTER(C.c_double), vp, vp, vp],
         "som_suggest_size": [i64, C.c_double, C.c_double, C.POINTER(i32), C.POINTER(i32),
                              C.POINTER(i64)],
@@ -248,10 +248,10 @@ def som_shuffle(seed: int, epoch: int, n: int):
 
 
 def som_train_plan(handle: int):
-    g, b, v = C.c_int32(), C.c_int32(), C.c_int32()
-    _check(lib().som_train_plan(handle, C.byref(g), C.byref(b), C.byref(v)),
+    g, b, v, m = C.c_int32(), C.c_int32(), C.c_int32(), C.c_int32()
+    _check(lib().som_train_plan(handle, C.byref(g), C.byref(b), C.byref(v), C.byref(m)),
            "som_train_plan")
-    return {"grid": g.value, "block": b.value, "variant": v.value}
+    return {"grid": g.value, "block": b.value, "variant": v.value, "block_steps": m.value}
 
 
 def som_pca2(X, n: int, d: int, stream=None, mean=None, v1=None, v2=None):

@@ -475,7 +475,7 @@ som_status som_init_linear(som_map *m, const float *X, int64_t n) {
 }
 
 som_status som_train_plan(const som_map *m, int32_t *grid, int32_t *block,
-                          int32_t *variant) {
+                          int32_t *variant, int32_t *block_steps) {
     if (!m) return SOM_E_ARG;
     som::TrainArgs a = train_args(const_cast<som_map *>(m), nullptr, 1);
     som::TrainPlan p;
@@ -485,6 +485,7 @@ som_status som_train_plan(const som_map *m, int32_t *grid, int32_t *block,
     if (grid) *grid = p.grid;
     if (block) *block = p.block;
     if (variant) *variant = p.variant;
+    if (block_steps) *block_steps = p.block_m;
     return SOM_OK;
 }
 

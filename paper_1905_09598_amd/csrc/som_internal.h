@@ -88,8 +88,7 @@ int64_t train_row_pitch(int32_t d);
 
 // Pipelined training (som_train_pipe.hip): estimated microseconds per step
 // of its best shape (1e300 if none fits), written into *plan.
-double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *plan,
-                       double (*exchange_us)(int));
+double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *plan);
 int64_t pipe_block_dots_floats(int m, int64_t nsteps);
 hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStream_t s);
 

@@ -513,7 +513,7 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
         TrainPlan pp;
         TrainArgs ap = a;
         ap.variant = a.variant >= 3 ? a.variant - 2 : 0;
-        const double tp = plan_train_pipe(ap, num_cus, max_lds, &pp, exchange_us_impl);
+        const double tp = plan_train_pipe(ap, num_cus, max_lds, &pp);
         if (tp < 1e300) {
             *plan = pp;
             return hipSuccess;

@@ -25,9 +25,11 @@ constexpr PipeInstance pipe_instance() {
 // up to 3 * 64 * KS float4).  The sample registers, 3 M KS float4 per lane,
 // bound M * KS: the longer blocks (8 x 2, 6 x 3, 4 x 4) and KS = 7 stay out
 // of scratch only in the LDS variant, which has no streamed row registers.
-// The planner takes the cheapest shape for the row length; a longer block
-// spreads the per-block work of the controller over more steps.  The
-// streamed kernels are listed in som_train_pipe_stream.hip.
+// The planner takes the cheapest shape for the row length: a longer block
+// spreads the per-block hand-over between sweepers and controller over more
+// steps, but its rows cost more per pass and its controller code (one
+// unrolled exchange per step) grows.  The streamed kernels are listed in
+// som_train_pipe_stream.hip.
 const PipeInstance kPipe[] = {
     pipe_instance<8, 1>(),        pipe_instance<4, 1>(),        pipe_instance<8, 2, false>(),
     pipe_instance<4, 2>(),        pipe_instance<6, 3, false>(), pipe_instance<4, 3>(),
@@ -49,10 +51,23 @@ size_t pipe_lds_bytes(int m, int rmax, int64_t P4, bool ldsw) {
     return b;
 }
 
+// Measured exchange latency of the pipelined kernel (multi-poll, per-XCD
+// replicated slots) by grid size, in microseconds.
+double pipe_exchange_us(int g) {
+    static const double gs[] = {1, 8, 64, 128, 256, 1024};
+    static const double us[] = {0.1, 1.02, 1.03, 1.07, 1.18, 2.0};
+    if (g <= 1) return us[0];
+    for (int i = 1; i < 6; ++i)
+        if (g <= gs[i]) {
+            const double f = (log2((double)g) - log2(gs[i - 1])) / (log2(gs[i]) - log2(gs[i - 1]));
+            return us[i - 1] + f * (us[i] - us[i - 1]);
+        }
+    return us[5];
+}
+
 }  // namespace
 
-double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *plan,
-                       double (*exchange_us)(int)) {
+double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *plan) {
     const int64_t P4 = a.ld / 4;
     if (P4 % 64 != 0) return 1e300;
     const int nsl = (int)(P4 / 64);
@@ -78,21 +93,23 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                     if (a.lds_rows >= 0) rl = a.lds_rows < rl ? a.lds_rows : rl;
                 }
                 if (rmax <= 64 && base <= (size_t)max_lds) {
-                    // Calibrated on MI355X.  Controller: about one exchange
-                    // plus 0.1 us per step and 1.2 us per block.  Sweeper:
-                    // a row slice costs ~(20 M + 4) VALU instructions and a
-                    // row ~(88 M + 400) cycles of reductions and coefficient
-                    // loads more (4 cycles per instruction at 2.4 GHz);
-                    // streamed rows add ~0.3 us of latency per row and take
-                    // at least the read and write of the workgroup's rows at
-                    // its share of 8 TB/s.
-                    const double item_us = (20.0 * pi.m + 4) * 4.0 / 2400.0;
-                    const double row_us = ks_need * item_us + (88.0 * pi.m + 400) / 2400.0;
-                    const double visit_us = rmax * row_us + (rmax - rl) * 0.3;
+                    // Calibrated on MI355X (LDS and streamed kernels, block
+                    // lengths 2 to 8, 2 to 256 workgroups).  Sweepers: one
+                    // pass over the rows per block, a row costing
+                    // KS (0.027 M + 0.04) + 0.012 M + 0.067 us, plus
+                    // 0.5 + 0.15 M us of hand-over per block and 0.05 us per
+                    // streamed row, and at least the read and write of the
+                    // streamed rows at the workgroup's share of 8 TB/s.
+                    // Controller: one exchange per step plus 0.03 M us
+                    // (longer blocks' larger unrolled code) and 0.36 us per
+                    // block.  A step takes the slower of the two.
+                    const double row_us = ks_need * (0.027 * pi.m + 0.0395) + 0.012 * pi.m + 0.0665;
+                    const double blk_us =
+                        rmax * row_us + (rmax - rl) * 0.05 + 0.5 + 0.15 * pi.m;
                     const double mem_us = (rmax - rl) * P4 * 32.0 / (8e6 / gg);
-                    const double sweep = (visit_us > mem_us ? visit_us : mem_us) / pi.m;
-                    const double ctl = exchange_us(gg) + 0.1;
-                    const double t = (sweep > ctl ? sweep : ctl) + 1.2 / pi.m;
+                    const double sweep = (blk_us > mem_us ? blk_us : mem_us) / pi.m;
+                    const double ctl = pipe_exchange_us(gg) + 0.03 * pi.m + 0.36 / pi.m;
+                    const double t = sweep > ctl ? sweep : ctl;
                     if (t < best) {
                         best = t;
                         plan->grid = gg;

@@ -64,7 +64,7 @@ def test_calls_on_null_map_are_argument_errors():
     assert L.som_topographic_error(None, None, 5, C.byref(v)) == 1
     assert L.som_destroy(None) == 0
     assert L.som_get_shape(None, None, None, None, None) == 1
-    assert L.som_train_plan(None, None, None, None) == 1
+    assert L.som_train_plan(None, None, None, None, None) == 1
 
 
 def test_shuffle_argument_errors():

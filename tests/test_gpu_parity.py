@@ -448,7 +448,7 @@ def test_pipelined_block_lengths_follow_the_oracle(rows, cols, d, n, epochs, blo
     monkeypatch.setenv("SOM_TRAIN_BLOCK_M", str(block_m))
     say("pipelined block length", block_m, "shape", rows, cols, d, n, epochs)
     plan = _train_vs_oracle(rows, cols, d, n, epochs)
-    assert plan["variant"] == 3
+    assert plan["variant"] == 3 and plan["block_steps"] == block_m
 
 
 @pytest.mark.parametrize("lds_rows", ["0", "1", "7", "64"])
