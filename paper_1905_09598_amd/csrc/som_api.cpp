@@ -380,8 +380,9 @@ static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
     const char *lr = getenv("SOM_TRAIN_LDS_ROWS");
     a.lds_rows = (lr && *lr) ? atoi(lr) : -1;
     if (a.lds_rows < -1) a.lds_rows = -1;
-    // SOM_TRAIN_BLOCK_M: steps per block of the pipelined kernel (a shape
-    // the build has for the row length; otherwise the other kernels run).
+    // SOM_TRAIN_BLOCK_M: steps per block (a pipelined shape the build has
+    // for the row length, else the blocked kernel's instance of that length
+    // if there is one, else the default choice).
     const char *bm = getenv("SOM_TRAIN_BLOCK_M");
     a.block_m = (bm && *bm) ? atoi(bm) : 0;
     if (a.block_m < 0) a.block_m = 0;

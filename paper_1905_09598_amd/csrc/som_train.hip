@@ -376,16 +376,23 @@ constexpr Instance instance() {
 }
 
 // Row pitch L * K float4 (d up to 4 L K floats) and block length M, sized so
-// the two blocks of samples (2 M K float4 per lane) stay in registers.
-// Per row length (lanes x k) the first instance is preferred; later ones of
-// the same row length (shorter blocks, less LDS per owned row) serve maps
-// whose workgroups own too many rows for the first.
+// the two blocks of samples (2 M K float4 per lane) stay in registers, the
+// longer rows' ones partly in the accumulation registers.  A longer block
+// reads and writes the streamed rows once for more steps (measured on
+// MI355X with 256 workgroups: 6.0k floats 4.96 -> 4.60 us per step from
+// M = 2 to 4, 8.0k 10.2 -> 7.7, 10k 13.7 -> 10.5 from M = 2 to 3, 12k and
+// 16k 28.8 -> 16.6 and 41.6 -> 23.1 from M = 1 to 2).  Per row length
+// (lanes x k) the first instance is preferred; later ones of the same row
+// length (shorter blocks, less LDS per owned row) serve maps whose
+// workgroups own too many rows for the first.
 const Instance kInstances[] = {
     instance<64, 1, 8, 1>(),   instance<64, 1, 4, 1>(),   instance<64, 1, 2, 1>(),
     instance<64, 2, 8, 1>(),   instance<64, 4, 4, 1>(),
     instance<128, 4, 4, 2>(),  instance<256, 3, 4, 1>(),  instance<256, 4, 4, 1>(),
-    instance<256, 5, 3, 1>(),  instance<256, 6, 2, 1>(),  instance<256, 8, 2, 1>(),
-    instance<256, 10, 2, 1>(), instance<256, 12, 1, 1>(), instance<256, 16, 1, 1>(),
+    instance<256, 5, 3, 1>(),  instance<256, 6, 4, 1>(),  instance<256, 6, 2, 1>(),
+    instance<256, 8, 4, 1>(),  instance<256, 8, 2, 1>(),  instance<256, 10, 3, 1>(),
+    instance<256, 10, 2, 1>(), instance<256, 12, 2, 1>(), instance<256, 12, 1, 1>(),
+    instance<256, 16, 2, 1>(), instance<256, 16, 1, 1>(),
 };
 
 const Instance *pick(int64_t ld4) {
@@ -445,16 +452,19 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
     if (e != hipSuccess) return e;
     const int max_grid = a.N < num_cus ? a.N : num_cus;
     // first instance of this row length whose per-row state fits in LDS at
-    // the largest grid (or the requested one)
+    // the largest grid (or the requested one), of the requested block
+    // length when the build has one that fits
     const Instance *in = nullptr;
     {
         const int g = a.grid > 0 ? (a.grid < a.N ? a.grid : a.N) : max_grid;
         const int rmax = (a.N + g - 1) / g;
-        for (const Instance &c : kInstances)
-            if ((int64_t)c.lanes * c.k == ld4 && lds_bytes_for(c, rmax, false) <= (size_t)max_lds) {
-                in = &c;
-                break;
-            }
+        for (int pass = a.block_m > 0 ? 0 : 1; pass < 2 && !in; ++pass)
+            for (const Instance &c : kInstances)
+                if ((int64_t)c.lanes * c.k == ld4 && (pass == 1 || c.m == a.block_m) &&
+                    lds_bytes_for(c, rmax, false) <= (size_t)max_lds) {
+                    in = &c;
+                    break;
+                }
     }
     if (!in) return hipErrorInvalidValue;
 

@@ -466,6 +466,28 @@ def test_streamed_variant_with_leading_rows_in_lds(rows, cols, d, n, epochs, lds
     assert plan["variant"] == 2 and plan["grid"] == 8
 
 
+# The blocked kernel's instances for rows too long for the pipelined one:
+# each row length's longest block and the shorter one kept for maps whose
+# workgroups own many rows.  Step counts leave a partial last block.
+@pytest.mark.parametrize("rows,cols,d,n,epochs,block_m", [
+    (5, 4, 6000, 31, 2, 4), (5, 4, 6000, 31, 2, 2),
+    (4, 5, 8000, 31, 1, 4), (4, 5, 8000, 31, 1, 2),
+    (4, 4, 9500, 31, 2, 3), (4, 4, 9500, 31, 2, 2),
+    (3, 5, 12000, 25, 1, 2), (3, 5, 12000, 25, 1, 1),
+    (3, 3, 16000, 17, 2, 2), (3, 3, 16000, 17, 2, 1),
+])
+@pytest.mark.parametrize("variant", ["1", "2"])
+def test_blocked_block_lengths_follow_the_oracle(rows, cols, d, n, epochs, block_m, variant,
+                                                 monkeypatch):
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", variant)
+    monkeypatch.setenv("SOM_TRAIN_BLOCK_M", str(block_m))
+    say("blocked block length", block_m, "variant", variant, "shape", rows, cols, d, n, epochs)
+    plan = _train_vs_oracle(rows, cols, d, n, epochs)
+    # SOM_TRAIN_VARIANT 1 asks for the LDS-resident rows (plan variant 1),
+    # 2 for the streamed ones (plan variant 0)
+    assert plan["variant"] == {"1": 1, "2": 0}[variant] and plan["block_steps"] == block_m
+
+
 @pytest.mark.parametrize("lds_rows", ["0", "1", "2", "64"])
 @pytest.mark.parametrize("rows,cols,d,n,epochs", [(6, 5, 3000, 30, 2), (5, 4, 9000, 20, 1)])
 def test_blocked_streamed_variant_with_leading_rows_in_lds(rows, cols, d, n, epochs, lds_rows,
