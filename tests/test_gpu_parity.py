@@ -466,6 +466,41 @@ def test_streamed_variant_with_leading_rows_in_lds(rows, cols, d, n, epochs, lds
     assert plan["variant"] == 2 and plan["grid"] == 8
 
 
+# The paper's own data shape (Table 1: several hundred short complaint
+# documents over about 4.5k terms, Sec. 6B) on a small map of both
+# lattices: TF-IDF rows of 637 x 4545 (23 terms each), 11 x 11 units.
+@pytest.mark.parametrize("topology", [som.RECT, som.HEX])
+def test_paper_shaped_tfidf_map_follows_the_oracle(topology):
+    rows = cols = 11
+    n, d, epochs = 637, 4545, 2
+    X = workloads.tfidf_like(n, d, 0.005, 8, seed=5)
+    order = workloads.epoch_orders(n, epochs, 5)
+    s = oracle.schedule(0.5, 0.01, 5.5, 1.0, oracle.LINEAR, oracle.EXPONENTIAL)
+    W0 = oracle.init_uniform(5, rows * cols, d)
+    say("paper-shaped map, topology", topology, "n", n, "d", d, "epochs", epochs)
+    m = som.Map(rows, cols, d, seed=5, topology=topology)
+    trace = dev(np.full(epochs * n, -1, np.int32))
+    m.train(dev(X), epochs, 0.5, 0.01, 5.5, 1.0, order=dev(order), bmu_trace=trace,
+            sigma_decay=som.EXPONENTIAL)
+    got = trace.cpu().numpy()
+    Wo, tr = oracle.train(W0, rows, cols, X, order, s, topology=topology, trace=True)
+    k = len(tr) if np.array_equal(got, tr) else int(np.argmax(got != tr))
+    say(f"  plan {m.plan()}: identical BMUs for {k}/{len(tr)} steps")
+    if k < len(tr):
+        Wk, _ = oracle.train(W0, rows, cols, X, order[:k], s, total_steps=epochs * n,
+                             topology=topology)
+        Ds = np.sort(oracle.distances(Wk, X[order[k]]))
+        assert (Ds[1] - Ds[0]) / Ds[0] <= GAP, "divergence without a near tie"
+    else:
+        err = np.abs(m.weights.cpu().numpy().astype(np.float64) - Wo).max()
+        say(f"  max|dW| = {err:.2e}")
+        assert err <= 1e-4
+    ev = oracle.evaluate(Wo, rows, cols, X, topology=topology)
+    qe = m.qe(dev(X))
+    assert abs(qe - ev["qe"]) <= 0.01 * ev["qe"]
+    m.close()
+
+
 # The blocked kernel's instances for rows too long for the pipelined one:
 # each row length's longest block and the shorter one kept for maps whose
 # workgroups own many rows.  Step counts leave a partial last block.
