@@ -87,42 +87,68 @@ __global__ __launch_bounds__(kEvalBlock) void bmu_candidates_kernel(EvalArgs a) 
         __syncthreads();
         if (tid < kBN) wn[tid] = (u0 + tid < u_end) ? a.wnorm[u0 + tid] : 0.f;
 
-        for (int k0 = 0; k0 < a.ld; k0 += kBK) {
-            __syncthreads();
-            // Stage X[s0 .. s0+kBM) x [k0, k0+kBK): 512 float4, two per thread.
+        // The next kBK-wide slices of X and W are loaded into registers
+        // before the current ones are multiplied, so their memory latency
+        // overlaps the MFMAs.  The loads are unconditional (addresses clamped
+        // into the operands); what lies outside them is zeroed as the slices
+        // go to LDS, after the multiply: a select on a value in flight would
+        // make the compiler wait for the load on the spot.
+        constexpr int kXPer = (kBM * kBK / 4) / kEvalBlock;  // float4 per thread
+        constexpr int kWPer = (kBN * kBK / 4) / kEvalBlock;
+        f4 xv[kXPer], wv[kWPer];
+        const auto fetch = [&](int k0) {
 #pragma unroll
-            for (int i = 0; i < (kBM * kBK / 4) / kEvalBlock; ++i) {
+            for (int i = 0; i < kXPer; ++i) {
                 const int idx = tid + i * kEvalBlock;
                 const int r = idx / (kBK / 4), c4 = idx % (kBK / 4);
-                const int64_t smp = s0 + r;
+                const int64_t smp = s0 + r < a.n ? s0 + r : a.n - 1;
+                const float *xr = a.X + smp * a.d;
                 const int64_t col = k0 + 4 * c4;
-                f4 v = {0.f, 0.f, 0.f, 0.f};
-                if (smp < a.n) {
-                    const float *xr = a.X + smp * a.d;
-                    if (a.x_vec4) {
-                        if (col < a.d) v = *reinterpret_cast<const f4 *>(xr + col);
-                    } else {
-                        v.x = (col + 0 < a.d) ? xr[col + 0] : 0.f;
-                        v.y = (col + 1 < a.d) ? xr[col + 1] : 0.f;
-                        v.z = (col + 2 < a.d) ? xr[col + 2] : 0.f;
-                        v.w = (col + 3 < a.d) ? xr[col + 3] : 0.f;
-                    }
+                if (a.x_vec4) {
+                    xv[i] = *reinterpret_cast<const f4 *>(xr + (col < a.d ? col : a.d - 4));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) xv[i][e] = xr[col + e < a.d ? col + e : a.d - 1];
                 }
+            }
+#pragma unroll
+            for (int i = 0; i < kWPer; ++i) {
+                const int idx = tid + i * kEvalBlock;
+                const int r = idx / (kBK / 4), c4 = idx % (kBK / 4);
+                const int64_t unit = u0 + r < u_end ? u0 + r : u_end - 1;
+                const int64_t col = k0 + 4 * c4;
+                wv[i] = *reinterpret_cast<const f4 *>(a.W + unit * a.ld +
+                                                      (col < a.ld ? col : a.ld - 4));
+            }
+        };
+        const auto stage = [&](int k0) {
+#pragma unroll
+            for (int i = 0; i < kXPer; ++i) {
+                const int idx = tid + i * kEvalBlock;
+                const int r = idx / (kBK / 4), c4 = idx % (kBK / 4);
+                const int64_t col = k0 + 4 * c4;
+                f4 v = xv[i];
+                const bool row_ok = s0 + r < a.n;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = (row_ok && col + e < a.d) ? v[e] : 0.f;
                 *reinterpret_cast<f4 *>(&xs[r * kLdsStride + 4 * c4]) = v;
             }
-            // Stage W[u0 .. u0+kBN) x [k0, k0+kBK): 1024 float4, four per thread.
 #pragma unroll
-            for (int i = 0; i < (kBN * kBK / 4) / kEvalBlock; ++i) {
+            for (int i = 0; i < kWPer; ++i) {
                 const int idx = tid + i * kEvalBlock;
                 const int r = idx / (kBK / 4), c4 = idx % (kBK / 4);
-                const int64_t unit = u0 + r;
                 const int64_t col = k0 + 4 * c4;
-                f4 v = {0.f, 0.f, 0.f, 0.f};
-                if (unit < u_end && col < a.ld)
-                    v = *reinterpret_cast<const f4 *>(a.W + unit * a.ld + col);
-                *reinterpret_cast<f4 *>(&ws[r * kLdsStride + 4 * c4]) = v;
+                const f4 zero = {0.f, 0.f, 0.f, 0.f};
+                *reinterpret_cast<f4 *>(&ws[r * kLdsStride + 4 * c4]) =
+                    (u0 + r < u_end && col < a.ld) ? wv[i] : zero;
             }
+        };
+        fetch(0);
+        for (int k0 = 0; k0 < a.ld; k0 += kBK) {
             __syncthreads();
+            stage(k0);
+            __syncthreads();
+            if (k0 + kBK < a.ld) fetch(k0 + kBK);
 
 #pragma unroll
             for (int kq = 0; kq < kBK; kq += 16) {
