@@ -28,7 +28,7 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 // 16 x 16.
 constexpr int kBM = 64;
 constexpr int kBN = 128;
-constexpr int kBK = 32;
+constexpr int kBK = 64;
 constexpr int kPad = 4;
 constexpr int kLdsStride = kBK + kPad;  // floats per staged row
 constexpr int kEvalBlock = 256;
@@ -57,7 +57,9 @@ __device__ inline void insert_top(float (&ts)[kCand], int (&tu)[kCand], float s,
     }
 }
 
-__global__ __launch_bounds__(kEvalBlock) void bmu_candidates_kernel(EvalArgs a) {
+// Two workgroups per compute unit (the register budget that allows, and the
+// planner's grid, assume it).
+__global__ __launch_bounds__(kEvalBlock, 2) void bmu_candidates_kernel(EvalArgs a) {
     __shared__ __align__(16) float xs[kBM * kLdsStride];
     __shared__ __align__(16) float ws[kBN * kLdsStride];
     __shared__ float wn[kBN];
