@@ -4,19 +4,31 @@
 One bench step is one pass of the whole hot path over the workload:
 reset the map to its seeded initial prototypes, train it for the workload's
 full schedule (epochs * n per-sample steps in one persistent kernel), then
-assign every sample to its BMU and compute QE and TE (batched MFMA BMU).
-Data, order and initial prototypes are resident in HBM before timing starts.
+assign every sample to its BMU and compute QE and TE (one batched MFMA BMU
+search, som_evaluate).  Data, order and initial prototypes are resident in
+HBM before timing starts.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload I] [--input csr]
 
-prints one JSON line.  --input csr trains from the CSR form of the same rows
-(som_train_csr, the sparse-input path) and reports that kernel's own bytes.  `value` is prototype*dim updates per second of the
-whole step, T * N * d / step time.  `roofline` reports the training call:
-algorithmic bytes 3 * N * d * 4 per sample (read the prototypes for the
-distance, read and write them for the update) divided by the average
-duration of som_train's kernels (schedule table, per-block sample products
-where used, the persistent training kernel) from HIP events on their
-stream, against the 8 TB/s HBM peak.
+prints one JSON line.  The default workload is the largest one, the
+100,000 x 2048 Gaussian mixture on a 100 x 100 map; the line also carries
+the 20,000 x 10,000 TF-IDF workload on a 50 x 50 map (`also`), the other
+workload the memory target is set on, timed over a few passes.  `value` is
+prototype*dim updates per second of the whole step, T * N * d / step time.
+
+`roofline` reports the training call: algorithmic bytes 3 * N * d * 4 per
+sample (read the prototypes for the distance, read and write them for the
+update) divided by the average duration of som_train's kernels from HIP
+events on their stream, against the 8 TB/s HBM peak (`frac`).  The blocked
+kernels move fewer bytes than that model (W streams once per block of
+steps, some rows stay in LDS), so `frac` can exceed 1; the memory the
+kernel really moves is `traffic` (FETCH_SIZE + WRITE_SIZE counters of the
+same kernel source, stored under profiles/), and `frac_applicable` is that
+traffic's rate against `stream_inplace`, an in-place stream over a buffer
+of W's size on the training grid measured in the same run.  `bound` comes
+from the launch plan: the LDS-resident kernels never stream W and wait on
+the grid exchange ("latency"), the streamed ones stream W once per block
+("hbm").
 `cpu_baseline` times the fp64 oracle on the host over a bounded prefix of
 the same training run.
 """
@@ -91,34 +103,62 @@ def cpu_baseline(cfg, X, order, budget_s: float, threads: int = 0):
     }
 
 
-def stream_reference(nbytes: int, reps: int = 5) -> dict:
-    """Same-footprint memory reference: c = a + b over three fp32 buffers of
-    nbytes each (two reads and one write per element, the access pattern of
-    the algorithmic 3 N d 4 bytes), best of reps, timed with HIP events on
-    the current stream.  Plain torch arithmetic: a bandwidth reference for
-    the roofline, not part of the SOM path."""
+def stream_inplace(nbytes: int, grid: int, target_ms: float = 40.0, reps: int = 3) -> dict:
+    """In-place stream over one device buffer of nbytes (som_stream_inplace:
+    each of `grid` workgroups reads and rewrites its own contiguous share,
+    many passes in one launch, no gaps), best of reps, HIP events on the
+    current stream.  A memory reference for the roofline, not a SOM step."""
     import torch
 
-    n = max(1, nbytes // 4)
-    a = torch.ones(n, dtype=torch.float32, device="cuda")
-    b = torch.ones(n, dtype=torch.float32, device="cuda")
-    c = torch.empty_like(a)
-    torch.add(a, b, out=c)
-    best, inner = None, 20
+    import paper_1905_09598_amd as som
+
+    nbytes = max(16, nbytes // 16 * 16)
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    st = torch.cuda.current_stream()
+    som.som_stream_inplace(buf, nbytes, 1, grid, st.cuda_stream)
+    # one pass moves 2 * nbytes; size the launch to about target_ms at 6 TB/s
+    passes = max(1, int(target_ms * 1e-3 * 6e12 / (2 * nbytes)))
+    best = None
     for _ in range(reps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(inner):
-            torch.add(a, b, out=c)
-        e1.record()
+        e0.record(st)
+        som.som_stream_inplace(buf, nbytes, passes, grid, st.cuda_stream)
+        e1.record(st)
         torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / inner
+        ms = e0.elapsed_time(e1)
         best = ms if best is None else min(best, ms)
-    return {"bytes": 3 * n * 4, "ms": best, "GB/s": 3 * n * 4 / (best / 1e3) / 1e9,
-            "what": f"c = a + b over three buffers the size of W (torch), {inner} launches "
-                    f"back to back, best of {reps}: the bandwidth a plain stream of the "
-                    "same footprint reaches, launch gaps included (L2 / MALL resident "
-                    "when W fits)"}
+    moved = 2.0 * nbytes * passes
+    del buf
+    return {"bytes": nbytes, "passes": passes, "grid": grid, "ms": best,
+            "GB/s": moved / (best / 1e3) / 1e9}
+
+
+def host_cpu() -> dict:
+    """The host's CPU model, physical cores and the cores this process may use."""
+    model, cores = None, set()
+    try:
+        phys = core = None
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                k, _, v = line.partition(":")
+                k, v = k.strip(), v.strip()
+                if k == "model name" and model is None:
+                    model = v
+                elif k == "physical id":
+                    phys = v
+                elif k == "core id":
+                    core = v
+                elif not k and phys is not None and core is not None:
+                    cores.add((phys, core))
+                    phys = core = None
+    except OSError:
+        pass
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        allowed = os.cpu_count()
+    return {"cpu_model": model, "physical_cores": len(cores) or None,
+            "sockets": len({p for p, _ in cores}) or None, "allowed_cores": allowed}
 
 
 def map_sweep(cpu_budget: float):
@@ -213,8 +253,14 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", type=int, default=1,
-                    help="index into the workload table (default: 2000 x 2000 TF-IDF)")
+    ap.add_argument("--workload", type=int, default=4,
+                    help="index into the workload table (default: the 100,000 x 2048 "
+                         "mixture on a 100 x 100 map)")
+    ap.add_argument("--also", type=str, default="3",
+                    help="comma-separated workload indices timed after the main one and "
+                         "reported under `also` ('' for none)")
+    ap.add_argument("--also-steps", type=int, default=3,
+                    help="timed passes of each `also` workload (after one warm-up)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--map-sweep", action="store_true",
@@ -257,10 +303,6 @@ def main():
               "8-byte arg-min exchange per step, which is not built)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
-    import torch
-
-    import paper_1905_09598_amd as som
     import workloads
 
     cfg = workloads.WORKLOADS[args.workload]
@@ -277,16 +319,67 @@ def main():
                  "map": f"{r}x{share // r}",
                  "note": "one GPU's share of the prototype rows, same samples, d and schedule; "
                          "the per-step arg-min exchange between GPUs is not built"}
+    import torch
+    torch.cuda.set_device(0)
+
+    res, X, order = measure(cfg, args.input, args.steps, args.warmup)
+    out = {
+        "metric": "SOM train prototype*dim updates/sec + % of HBM/MALL roofline, 1 MI355X",
+        "value": res.pop("value"),
+        "unit": "proto*dim updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": res.pop("ms_per_step"),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": res.pop("config"),
+    }
+    out.update(res)
+    if shard:
+        out["config"]["shard"] = shard
+    if args.cpu_budget > 0:
+        host = host_cpu()
+        out["cpu_baseline"] = cpu_baseline(cfg, X, order, args.cpu_budget)
+        out["cpu_baseline"]["host"] = host
+        # the same oracle on one core (a third of the budget), for the
+        # single-core speed-up
+        out["cpu_baseline_1core"] = cpu_baseline(cfg, X, order, args.cpu_budget / 3, threads=1)
+    del X, order
+    also = [int(t) for t in args.also.split(",") if t.strip()] if not shard else []
+    if also:
+        out["also"] = {}
+        for wi in also:
+            if wi == args.workload:
+                continue
+            c = workloads.WORKLOADS[wi]
+            r, Xa, _ = measure(c, args.input, args.also_steps, 1)
+            out["also"][c.name] = r
+            del Xa
+    print(json.dumps(out), flush=True)
+
+
+def measure(cfg, input_kind: str, steps: int, warmup: int):
+    """Time `steps` bench steps of one workload (after `warmup`); returns
+    (result fields, X, order)."""
+    import numpy as np
+    import torch
+
+    import paper_1905_09598_amd as som
+    import workloads
+
     X = workloads.make_data(cfg)
     order = workloads.epoch_orders(cfg.n, cfg.epochs, cfg.shuffle_seed)
-    torch.cuda.set_device(0)
     Xd = torch.from_numpy(X).cuda()
     od = torch.from_numpy(order).cuda()
     m = som.Map(cfg.rows, cfg.cols, cfg.d, seed=cfg.init_seed)
     W0 = m.weights.clone()
     plan = m.plan()
     stream = torch.cuda.current_stream()
-    sparse = args.input == "csr"
+    sparse = input_kind == "csr"
     if sparse:
         # CSR form of the same rows (host-side input preparation, untimed)
         nz = X != 0
@@ -310,19 +403,18 @@ def main():
             m.train(Xd, cfg.epochs, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1, order=od)
         if ev is not None:
             ev[1].record(stream)
-        idx = m.bmu(Xd)
-        qe, te = m.qe(Xd), m.te(Xd)
-        return idx, qe, te
+        # every sample's BMU, QE and TE from one batched BMU search
+        return m.evaluate(Xd)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         one_step()
     torch.cuda.synchronize()
 
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
+              for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for k in range(args.steps):
+    for k in range(steps):
         _, qe, te = one_step(events[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -342,7 +434,7 @@ def main():
     bmu_flops = 2.0 * cfg.n * cfg.units * cfg.d
     avg_train_s = sum(train_ms) / len(train_ms) / 1e3
     updates = cfg.steps * cfg.units * cfg.d
-    ms_per_step = wall / args.steps * 1e3
+    ms_per_step = wall / steps * 1e3
     alg_bytes = cfg.steps * 3.0 * cfg.units * cfg.d * 4
     achieved = alg_bytes / avg_train_s / 1e9
     traffic = measured_traffic(cfg.name)
@@ -350,6 +442,9 @@ def main():
                    "train_pipe_kernel (stream)", "train_pipe_kernel (lds)"][plan["variant"]]
     variant = ["stream", "lds", "pipelined-stream", "pipelined-lds"][plan["variant"]]
     grid, block = plan["grid"], plan["block"]
+    # the LDS-resident kernels keep W on chip and wait on the grid exchange;
+    # the streamed ones read and write W once per block of steps
+    bound = "hbm" if plan["variant"] in (0, 2) else "latency"
     if sparse:
         # the sparse path's own bytes: the dense 3 N d 4 per step does not
         # describe a kernel that touches only the sample's features
@@ -359,39 +454,43 @@ def main():
         kernel_name = "sparse_train_kernel"
         variant = "csr lazy-scale"
         grid, block = -(-cfg.units // 64), 128
-
-    out = {
-        "metric": "SOM train prototype*dim updates/sec + % of HBM/MALL roofline, 1 MI355X",
+        bound = "latency"
+    ref = stream_inplace(cfg.units * cfg.d * 4, grid if not sparse else 256)
+    roof = {
+        "bound": bound,
+        "achieved": achieved,
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": achieved / HBM_PEAK_GBS,
+        "traffic": traffic,
+        "kernel": kernel_name,
+        "kernel_ms": avg_train_s * 1e3,
+        "alg_bytes_per_launch": alg_bytes,
+        "stream_inplace": ref,
+    }
+    if traffic:
+        phys = traffic / avg_train_s / 1e9
+        roof["traffic_source"] = ("FETCH_SIZE + WRITE_SIZE of this kernel source on this "
+                                  "workload, stored in profiles/train_kernel_traffic.json")
+        roof["traffic_GBs"] = phys
+        roof["frac_hbm_traffic"] = phys / HBM_PEAK_GBS
+        roof["frac_applicable"] = phys / ref["GB/s"]
+    if sparse:
+        roof["note"] = ("sparse path: bytes = the samples' non-zeros gathered and scattered in "
+                        "fp64 for every unit; its step is bound by the grid exchange's latency, "
+                        "not by bytes")
+    res = {
         "value": updates / (ms_per_step / 1e3),
-        "unit": "proto*dim updates/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
         "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
         "config": {
             "workload": cfg.name, "n": cfg.n, "d": cfg.d,
             "map": f"{cfg.rows}x{cfg.cols}", "epochs": cfg.epochs,
             "train_steps_per_pass": cfg.steps,
             "schedule": f"lr {cfg.lr0}->{cfg.lr1} linear, sigma {cfg.sigma0}->{cfg.sigma1} exp",
-            "grid": grid, "block": block, "variant": variant, "input": args.input,
+            "grid": grid, "block": block, "variant": variant, "input": input_kind,
             "block_steps": None if sparse else plan["block_steps"],
         },
-        "roofline": {
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
-            "traffic": traffic,
-            "kernel": kernel_name,
-            "kernel_ms": avg_train_s * 1e3,
-            "alg_bytes_per_launch": alg_bytes,
-        },
+        "roofline": roof,
         "bmu_mfma": {
             "achieved": bmu_flops / bmu_s / 1e12, "peak": FP32_MFMA_PEAK_TFLOPS,
             "unit": "TFLOP/s", "frac": bmu_flops / bmu_s / 1e12 / FP32_MFMA_PEAK_TFLOPS,
@@ -404,20 +503,10 @@ def main():
         "qe": qe,
         "te": te,
     }
-    if shard:
-        out["config"]["shard"] = shard
-    if sparse:
-        out["roofline"]["note"] = ("sparse path: bytes = the samples' non-zeros gathered and "
-                                   "scattered in fp64 for every unit; its step is bound by the "
-                                   "grid exchange's latency, not by bytes")
-    out["stream_reference"] = stream_reference(cfg.units * cfg.d * 4)
-    if args.cpu_budget > 0:
-        out["cpu_baseline"] = cpu_baseline(cfg, X, order, args.cpu_budget)
-        # the same oracle on one core (a third of the budget), for the
-        # single-core speed-up
-        out["cpu_baseline_1core"] = cpu_baseline(cfg, X, order, args.cpu_budget / 3, threads=1)
-    print(json.dumps(out), flush=True)
     m.close()
+    del Xd, od, W0
+    torch.cuda.empty_cache()
+    return res, X, order
 
 
 if __name__ == "__main__":

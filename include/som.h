@@ -30,8 +30,16 @@
  *     out) is reported by the next synchronizing call on that map.
  *   - A map is not thread-safe: use one map per host thread.
  *   - Floating point: prototypes and data are fp32; distances are fp32 sums;
- *     the schedule and the neighbourhood factors are evaluated in fp64 and
- *     rounded once to fp32; QE and TE are accumulated in fp64.
+ *     the schedule (lr and log2(e) / (2 sigma^2) per step) is evaluated in
+ *     fp64 and rounded once to fp32; the neighbourhood factor of every unit
+ *     is then lr * exp2(-g * log2(e) / (2 sigma^2)) in fp32 (the hardware
+ *     exp2, denormal results flushed to zero), g the squared lattice
+ *     distance; QE and TE are accumulated in fp64.
+ *   - Device pointer extents are checked against the allocation that holds
+ *     the pointer (hipMemGetAddressRange).  Under a pooling allocator (for
+ *     example torch's caching allocator) that allocation can be a larger
+ *     pool segment, so the check is best effort: a pointer whose own tensor
+ *     is shorter than the stated extent can still pass it.
  */
 #ifndef SOM_H
 #define SOM_H
@@ -213,6 +221,18 @@ som_status som_quantization_error(som_map *map, const float *X, int64_t n,
 som_status som_topographic_error(som_map *map, const float *X, int64_t n,
                                  double *out_te);
 
+/* Evaluation in one pass (Sec. 8A, Sec. 6D, Sec. 8B): the BMU of every
+ * one of the n rows of the device matrix X into out_idx (a device int32
+ * array of n entries, or NULL), together with the quantization error
+ * (*out_qe) and the topographic error (*out_te) of som_quantization_error
+ * and som_topographic_error, from one batched BMU search instead of one
+ * per quantity.  out_qe and out_te are host doubles; either may be NULL,
+ * but not all three outputs.  Synchronizes the stream.
+ * Errors: SOM_E_ARG (map or X NULL, n <= 0 or above 2^31 - 1, X or out_idx
+ * not covering their extent, all outputs NULL), SOM_E_OOM, SOM_E_DEVICE. */
+som_status som_evaluate(som_map *map, const float *X, int64_t n, int32_t *out_idx,
+                        double *out_qe, double *out_te);
+
 /* Copy the rows*cols x d prototypes (row-major, unit u = r * cols + c) out
  * to / in from `dst` / `src`, a host or device pointer of rows*cols*d floats.
  * Used to start from a given state and to checkpoint and resume.
@@ -277,6 +297,22 @@ som_status som_init_linear(som_map *map, const float *X, int64_t n);
  * updates one pass over the prototypes applies).  Any output may be NULL. */
 som_status som_train_plan(const som_map *map, int32_t *grid, int32_t *block,
                           int32_t *variant, int32_t *block_steps);
+
+/* Memory reference for the roofline of som_train; not a step of the
+ * method.  Rewrites the `bytes` bytes at the device pointer buf in place,
+ * `passes` times, in one launch of `grid` workgroups of 256 threads:
+ * workgroup b of G reads, scales by 1 and writes back its own contiguous
+ * share of the buffer's 16-byte words (b / G to (b + 1) / G of them), as a
+ * training workgroup streams its own range of prototype rows, so no
+ * workgroup waits for another and the passes follow each other without a
+ * gap.  The buffer's contents are unchanged.  Moves 2 * bytes * passes
+ * bytes.  Ordered on `stream` (a hipStream_t, NULL for the null stream);
+ * returns after enqueueing.
+ * Errors: SOM_E_ARG (buf NULL or not 16-byte aligned, bytes <= 0 or not a
+ * multiple of 16, passes <= 0, grid outside [1, 1024], buf not covering
+ * `bytes`), SOM_E_DEVICE. */
+som_status som_stream_inplace(void *buf, int64_t bytes, int32_t passes, int32_t grid,
+                              void *stream);
 
 /* Human-readable name of a status code (static storage). */
 const char *som_status_string(som_status status);

@@ -69,6 +69,11 @@ def lib():
                                        C.c_int64, C.c_int64, C.POINTER(Schedule),
                                        ip, C.c_int]
         L.som_oracle_train.restype = C.c_int
+        L.som_oracle_train_near_tie.argtypes = [
+            dp, C.c_int32, C.c_int32, C.c_int32, C.c_int64, fp, C.c_int64, ip,
+            C.c_int64, C.c_int64, C.c_int64, C.POINTER(Schedule), C.c_double,
+            C.c_uint64, C.POINTER(C.c_int64), C.c_int]
+        L.som_oracle_train_near_tie.restype = C.c_int
         L.som_oracle_evaluate.argtypes = [dp, C.c_int32, C.c_int32, C.c_int32,
                                           C.c_int64, fp, C.c_int64, ip, ip, dp,
                                           dp, dp, dp, C.c_int]
@@ -165,6 +170,30 @@ def train(W: np.ndarray, rows: int, cols: int, X: np.ndarray,
     if rc != 0:
         raise ValueError(f"som_oracle_train: bad arguments (rc={rc})")
     return W, tr
+
+
+def train_near_tie(W: np.ndarray, rows: int, cols: int, X: np.ndarray,
+                   order: np.ndarray, s: Schedule, tie_rel: float, seed: int,
+                   step0: int = 0, total_steps: Optional[int] = None,
+                   topology: int = RECT, nthreads: Optional[int] = None):
+    """train() with every near tie (D2 - D1 <= tie_rel * D1) decided by a
+    seeded coin; returns (W, number of steps that took the second unit)."""
+    W = np.array(W, dtype=np.float64, order="C", copy=True)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    order = np.ascontiguousarray(order, dtype=np.int32)
+    n, d = X.shape
+    assert W.shape == (rows * cols, d)
+    nsteps = order.shape[0]
+    T = step0 + nsteps if total_steps is None else int(total_steps)
+    flips = C.c_int64()
+    rc = lib().som_oracle_train_near_tie(
+        _p(W, C.c_double), rows, cols, topology, d, _p(X, C.c_float), n,
+        _p(order, C.c_int32), nsteps, step0, T, C.byref(s), float(tie_rel),
+        C.c_uint64(seed), C.byref(flips),
+        default_threads() if nthreads is None else nthreads)
+    if rc != 0:
+        raise ValueError(f"som_oracle_train_near_tie: bad arguments (rc={rc})")
+    return W, flips.value
 
 
 def evaluate(W: np.ndarray, rows: int, cols: int, X: np.ndarray,

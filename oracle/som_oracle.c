@@ -273,6 +273,75 @@ int som_oracle_train(double *W, int32_t rows, int32_t cols, int32_t topology,
 }
 
 /* ------------------------------------------------------------------------
+ * Training with near ties decided by a coin.  The same online steps as
+ * som_oracle_train, except at a step whose second-smallest distance D2
+ * exceeds the smallest D1 by at most tie_rel * D1: there the BMU is the
+ * first or the second unit as bit 63 of SplitMix64(seed, global step) says
+ * (1 = the second).  Two units that close are a tie at any precision that
+ * cannot resolve tie_rel, so each such training is as valid as the plain
+ * one; an ensemble of them over seeds measures how far the end of training
+ * moves when runs part at near ties.  With tie_rel = 0 only exact ties
+ * (D2 = D1) are candidates, and those flip too.  *flips (nullable) receives
+ * the number of steps at which the second unit was taken.
+ * ---------------------------------------------------------------------- */
+int som_oracle_train_near_tie(double *W, int32_t rows, int32_t cols, int32_t topology,
+                              int64_t d, const float *X, int64_t n, const int32_t *order,
+                              int64_t nsteps, int64_t step0, int64_t total_steps,
+                              const som_oracle_schedule *s, double tie_rel,
+                              uint64_t seed, int64_t *flips, int nthreads)
+{
+    if (!W || !X || !order || !s || rows <= 0 || cols <= 0 || d <= 0 || n <= 0 ||
+        nsteps < 0 || step0 < 0 || total_steps < step0 + nsteps || !(tie_rel >= 0.0))
+        return ORACLE_E_ARG;
+    if (nthreads < 1)
+        nthreads = 1;
+    int64_t N = (int64_t)rows * cols;
+    double *x = (double *)malloc((size_t)d * sizeof(double));
+    double *D = (double *)malloc((size_t)N * sizeof(double));
+    double *h = (double *)malloc((size_t)N * sizeof(double));
+    if (!x || !D || !h) {
+        free(x); free(D); free(h);
+        return ORACLE_E_ARG;
+    }
+    int64_t nflip = 0;
+    for (int64_t k = 0; k < nsteps; ++k) {
+        int64_t i = order[k];
+        if (i < 0 || i >= n) {
+            free(x); free(D); free(h);
+            return ORACLE_E_ARG;
+        }
+        for (int64_t j = 0; j < d; ++j)
+            x[j] = (double)X[i * d + j];
+        double lr, sigma;
+        som_oracle_schedule_at(step0 + k, total_steps, s, &lr, &sigma);
+
+        oracle_distances(W, N, d, x, D, nthreads);
+        int64_t c = oracle_argmin(D, N, -1);
+        if (N > 1) {
+            int64_t c2 = oracle_argmin(D, N, c);
+            if (D[c2] - D[c] <= tie_rel * D[c] &&
+                (oracle_splitmix64(seed, (uint64_t)(step0 + k)) >> 63)) {
+                c = c2;
+                ++nflip;
+            }
+        }
+
+        som_oracle_neighbourhood(rows, cols, topology, c, lr, sigma, h);
+#pragma omp parallel for schedule(static) num_threads(nthreads) if (nthreads > 1)
+        for (int64_t u = 0; u < N; ++u) {
+            double *w = W + u * d;
+            double hu = h[u];
+            for (int64_t j = 0; j < d; ++j)
+                w[j] = w[j] + hu * (x[j] - w[j]);
+        }
+    }
+    if (flips)
+        *flips = nflip;
+    free(x); free(D); free(h);
+    return ORACLE_OK;
+}
+
+/* ------------------------------------------------------------------------
  * Evaluation over all n samples with fixed weights: first and second BMU,
  * their squared distances, quantization error and topographic error.
  * Any output pointer may be NULL.

@@ -27,7 +27,7 @@ __all__ = [
     "som_train", "som_train_csr", "som_train_batch", "som_bmu", "som_bmu2",
     "som_quantization_error", "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
-    "som_pca2", "som_suggest_size", "som_init_linear",
+    "som_pca2", "som_suggest_size", "som_init_linear", "som_evaluate", "som_stream_inplace",
     "som_status_string", "RECT", "HEX", "LINEAR", "EXPONENTIAL", "EXPORTED",
 ]
 
@@ -47,7 +47,8 @@ EXPORTED = (
     "som_train", "som_train_csr", "som_train_batch", "som_bmu", "som_bmu2", "som_quantization_error",
     "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
-    "som_pca2", "som_suggest_size", "som_init_linear", "som_status_string",
+    "som_pca2", "som_suggest_size", "som_init_linear", "som_evaluate", "som_stream_inplace",
+    "som_status_string",
 )
 
 
@@ -113,6 +114,8 @@ def lib():
         "som_suggest_size": [i64, C.c_double, C.c_double, C.POINTER(i32), C.POINTER(i32),
                              C.POINTER(i64)],
         "som_init_linear": [vp, vp, i64],
+        "som_evaluate": [vp, vp, i64, vp, C.POINTER(C.c_double), C.POINTER(C.c_double)],
+        "som_stream_inplace": [vp, i64, i32, i32, vp],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -274,6 +277,20 @@ def som_init_linear(handle: int, X, n: int) -> None:
     _check(lib().som_init_linear(handle, _ptr(X), n), "som_init_linear")
 
 
+def som_evaluate(handle: int, X, n: int, out_idx=None):
+    """(QE, TE) of the n rows of X from one BMU search; the BMUs go to
+    out_idx when given."""
+    qe, te = C.c_double(), C.c_double()
+    _check(lib().som_evaluate(handle, _ptr(X), n, _ptr(out_idx), C.byref(qe), C.byref(te)),
+           "som_evaluate")
+    return qe.value, te.value
+
+
+def som_stream_inplace(buf, nbytes: int, passes: int, grid: int, stream=None) -> None:
+    _check(lib().som_stream_inplace(_ptr(buf), int(nbytes), int(passes), int(grid), stream),
+           "som_stream_inplace")
+
+
 def som_status_string(code: int) -> str:
     return lib().som_status_string(code).decode()
 
@@ -333,9 +350,7 @@ class Map:
               sigma1: float, lr_decay: int = LINEAR,
               sigma_decay: int = EXPONENTIAL, order=None, shuffle_seed: int = 0,
               step0: int = 0, total_steps: int = 0, bmu_trace=None) -> None:
-        _require(X, "float32", "X")
-        if X.dim() != 2 or X.shape[1] != self.d:
-            raise ValueError(f"X must be (n, {self.d})")
+        self._check_x(X)
         if order is not None:
             _require(order, "int32", "order")
         if bmu_trace is not None:
@@ -373,14 +388,12 @@ class Map:
     def train_batch(self, X, epochs: int, sigma0: float, sigma1: float,
                     sigma_decay: int = EXPONENTIAL) -> None:
         """Batch-map epochs over the rows of X (see som_train_batch)."""
-        _require(X, "float32", "X")
-        if X.dim() != 2 or X.shape[1] != self.d:
-            raise ValueError(f"X must be (n, {self.d})")
+        self._check_x(X)
         self._bind_stream()
         som_train_batch(self.handle, X, X.shape[0], int(epochs), sigma0, sigma1, sigma_decay)
 
     def bmu(self, X, second: bool = False):
-        _require(X, "float32", "X")
+        self._check_x(X)
         torch = self._torch
         n = X.shape[0]
         idx = torch.empty(n, dtype=torch.int32, device=X.device)
@@ -393,15 +406,30 @@ class Map:
         som_bmu2(self.handle, X, n, idx, idx2, d1)
         return idx, idx2, d1
 
-    def qe(self, X) -> float:
+    def _check_x(self, X):
         _require(X, "float32", "X")
+        if X.dim() != 2 or X.shape[1] != self.d:
+            raise ValueError(f"X must be (n, {self.d})")
+
+    def qe(self, X) -> float:
+        self._check_x(X)
         self._bind_stream()
         return som_quantization_error(self.handle, X, X.shape[0])
 
     def te(self, X) -> float:
-        _require(X, "float32", "X")
+        self._check_x(X)
         self._bind_stream()
         return som_topographic_error(self.handle, X, X.shape[0])
+
+    def evaluate(self, X, with_bmu: bool = True):
+        """(BMUs or None, QE, TE) of the rows of X from one BMU search."""
+        self._check_x(X)
+        idx = None
+        if with_bmu:
+            idx = self._torch.empty(X.shape[0], dtype=self._torch.int32, device=X.device)
+        self._bind_stream()
+        qe, te = som_evaluate(self.handle, X, X.shape[0], idx)
+        return idx, qe, te
 
     @property
     def weights(self):
@@ -429,6 +457,6 @@ class Map:
 
     def init_linear(self, X) -> None:
         """Prototypes on the plane of X's two largest principal components."""
-        _require(X, "float32", "X")
+        self._check_x(X)
         self._bind_stream()
         som_init_linear(self.handle, X, X.shape[0])

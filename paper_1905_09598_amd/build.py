@@ -21,7 +21,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libsom.so")
 SOURCES = ["som_api.cpp", "som_train.hip", "som_train_pipe.hip", "som_train_pipe_stream.hip",
-           "som_eval.hip", "som_util.hip", "som_pca.hip", "som_sparse.hip", "som_batch.hip"]
+           "som_eval.hip", "som_util.hip", "som_pca.hip", "som_sparse.hip", "som_batch.hip",
+           "som_stream.hip"]
 ARCH = "gfx950"
 
 

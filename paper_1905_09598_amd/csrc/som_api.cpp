@@ -168,16 +168,22 @@ hipError_t ensure(som_map *m, T **p, int64_t *cap, int64_t need) {
     return e;
 }
 
+// Evaluation scratch for n samples and ncand candidates.  A capacity is
+// zeroed before its buffers are replaced and set again only once every one
+// of them is allocated, so a failed allocation leaves no stale capacity
+// behind a null or freed buffer.
 som_status ensure_eval_scratch(som_map *m, int64_t n, int64_t ncand) {
     hipError_t e;
     som_status st;
     if (ncand > m->cand_cap) {
         if ((e = hipStreamSynchronize(m->stream)) != hipSuccess) return from_hip(e);
+        m->cand_cap = 0;
         if ((st = grow(&m->cand, ncand)) != SOM_OK) return st;
         m->cand_cap = ncand;
     }
     if (n <= m->eval_cap) return SOM_OK;
     if ((e = hipStreamSynchronize(m->stream)) != hipSuccess) return from_hip(e);
+    m->eval_cap = 0;
     if ((st = grow(&m->idx1, n)) != SOM_OK) return st;
     if ((st = grow(&m->idx2, n)) != SOM_OK) return st;
     if ((st = grow(&m->d1, n)) != SOM_OK) return st;
@@ -767,14 +773,16 @@ som_status som_bmu(som_map *m, const float *X, int64_t n, int32_t *out_idx) {
     return som_bmu2(m, X, n, out_idx, nullptr, nullptr);
 }
 
-static som_status qe_te(som_map *m, const float *X, int64_t n, double *qe, double *te) {
+static som_status qe_te(som_map *m, const float *X, int64_t n, int32_t *out_idx, double *qe,
+                        double *te) {
     if (!eval_args_ok(m, X, n)) return SOM_E_ARG;
+    if (out_idx && !device_range_ok(out_idx, (uint64_t)n * 4)) return SOM_E_ARG;
     som_status st = ensure_eval_scratch(m, n, 0);
     if (st != SOM_OK) return st;
-    st = run_eval(m, X, n, m->idx1, m->idx2, m->d1);
+    st = run_eval(m, X, n, out_idx ? out_idx : m->idx1, m->idx2, m->d1);
     if (st != SOM_OK) return st;
-    hipError_t e = som::launch_qe_te_reduce(m->idx1, m->idx2, m->d1, n, m->cols,
-                                            m->topology, m->sums, m->stream);
+    hipError_t e = som::launch_qe_te_reduce(out_idx ? out_idx : m->idx1, m->idx2, m->d1, n,
+                                            m->cols, m->topology, m->sums, m->stream);
     double h[2] = {0.0, 0.0};
     if (e == hipSuccess)
         e = hipMemcpyAsync(h, m->sums, sizeof(h), hipMemcpyDeviceToHost, m->stream);
@@ -789,12 +797,29 @@ static som_status qe_te(som_map *m, const float *X, int64_t n, double *qe, doubl
 
 som_status som_quantization_error(som_map *m, const float *X, int64_t n, double *out_qe) {
     if (!out_qe) return SOM_E_ARG;
-    return qe_te(m, X, n, out_qe, nullptr);
+    return qe_te(m, X, n, nullptr, out_qe, nullptr);
 }
 
 som_status som_topographic_error(som_map *m, const float *X, int64_t n, double *out_te) {
     if (!out_te) return SOM_E_ARG;
-    return qe_te(m, X, n, nullptr, out_te);
+    return qe_te(m, X, n, nullptr, nullptr, out_te);
+}
+
+som_status som_evaluate(som_map *m, const float *X, int64_t n, int32_t *out_idx,
+                        double *out_qe, double *out_te) {
+    if (!out_qe && !out_te && !out_idx) return SOM_E_ARG;
+    return qe_te(m, X, n, out_idx, out_qe, out_te);
+}
+
+som_status som_stream_inplace(void *buf, int64_t bytes, int32_t passes, int32_t grid,
+                              void *stream) {
+    if (!buf || bytes <= 0 || bytes % 16 != 0 || passes <= 0 || grid <= 0 ||
+        grid > som::kMaxTrainGrid)
+        return SOM_E_ARG;
+    if (reinterpret_cast<uintptr_t>(buf) % 16 != 0) return SOM_E_ARG;
+    if (!device_range_ok(buf, (uint64_t)bytes)) return SOM_E_ARG;
+    return from_hip(som::launch_stream_inplace(static_cast<float *>(buf), bytes, passes, grid,
+                                               1.0f, reinterpret_cast<hipStream_t>(stream)));
 }
 
 som_status som_get_weights(som_map *m, float *dst) {

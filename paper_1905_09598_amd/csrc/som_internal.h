@@ -189,6 +189,11 @@ struct BatchArgs {
 size_t batch_work_doubles(int32_t rows, int32_t cols, int32_t d, int32_t topology);
 hipError_t launch_batch_epoch(const BatchArgs &b, hipStream_t s);
 
+// In-place stream over `bytes` (a multiple of 16) of buf on `grid`
+// workgroups, `passes` times, each word scaled by a (som_stream.hip).
+hipError_t launch_stream_inplace(float *buf, int64_t bytes, int32_t passes, int32_t grid,
+                                 float a, hipStream_t s);
+
 // Principal components and linear initialisation (som_pca.hip).
 constexpr int kPcaBlock = 8;  // subspace-iteration block
 // Floats of work memory for pca_top2 (covariance d x d, iteration vectors,

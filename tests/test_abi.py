@@ -65,6 +65,9 @@ def test_calls_on_null_map_are_argument_errors():
     assert L.som_destroy(None) == 0
     assert L.som_get_shape(None, None, None, None, None) == 1
     assert L.som_train_plan(None, None, None, None, None) == 1
+    assert L.som_evaluate(None, None, 5, None, C.byref(v), None) == 1
+    assert L.som_stream_inplace(None, 16, 1, 1, None) == 1
+    assert L.som_stream_inplace(None, 15, 1, 1, None) == 1
 
 
 def test_shuffle_argument_errors():

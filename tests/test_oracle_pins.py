@@ -306,11 +306,73 @@ def test_quantization_error_non_increasing_on_separated_mixture():
     assert qes[-1] < 0.1 * qes[0]
 
 
+# ------------------------------------------------- near-tie coin trainings
+def test_near_tie_training_without_ties_is_the_plain_training():
+    """With tie_rel = 0 only exact ties are coin candidates; on data with
+    none, every seed reproduces the plain training bit for bit."""
+    X = gaussian_mixture(64, 24, 4, 0.1, seed=3)
+    W0 = oracle.init_uniform(1, 25, 24)
+    order = epoch_orders(64, 3, seed=2)
+    s = oracle.schedule(0.5, 0.01, 3.0, 0.5)
+    Wa, _ = oracle.train(W0, 5, 5, X, order, s)
+    for seed in (0, 1, 99):
+        Wb, flips = oracle.train_near_tie(W0, 5, 5, X, order, s, 0.0, seed)
+        assert flips == 0 and np.array_equal(Wa, Wb)
+
+
+def test_near_tie_training_flips_exact_ties_by_the_published_generator():
+    """Two identical prototypes tie exactly at every step.  With sigma = 0
+    and lr = 1 the chosen unit becomes the sample; the plain rule always
+    takes unit 0, the coin rule takes unit 1 exactly at the steps whose
+    SplitMix64 output (checked against its published values elsewhere) has
+    its top bit set."""
+    X = np.array([[1.0, 2.0], [3.0, -1.0], [0.5, 0.25]], dtype=np.float32)
+    W0 = np.zeros((2, 2))
+    s = sched(1.0, 0.0)
+    seed = 12345
+    bits = oracle.splitmix64(seed, 64) >> np.uint64(63)
+    for t in range(40):
+        order = np.array([t % 3], dtype=np.int32)
+        W, flips = oracle.train_near_tie(W0, 1, 2, X, order, s, 0.0, seed, step0=t,
+                                         total_steps=64)
+        moved = 1 if bits[t] else 0
+        assert flips == moved
+        assert np.array_equal(W[moved], X[t % 3].astype(np.float64))
+        assert np.array_equal(W[1 - moved], W0[1 - moved])
+        Wp, _ = oracle.train(W0, 1, 2, X, order, s, step0=t, total_steps=64)
+        assert np.array_equal(Wp[0], X[t % 3].astype(np.float64))
+
+
+def test_near_tie_threshold_is_relative_to_the_smaller_distance():
+    """A 1 x 2 map whose units sit at squared distances 1 and 1 + 1e-7 from
+    the sample: a near tie for tie_rel >= 1e-7, not for 1e-8."""
+    X = np.zeros((1, 1), dtype=np.float32)
+    W0 = np.array([[1.0], [-math.sqrt(1.0 + 1e-7)]])
+    D = oracle.distances(W0, X[0])
+    rel = (D[1] - D[0]) / D[0]
+    assert 0.99e-7 < rel < 1.01e-7
+    s = sched(1.0, 0.0)
+    bits = oracle.splitmix64(7, 32) >> np.uint64(63)
+    order = np.zeros(32, dtype=np.int32)
+    # lr = 1, sigma = 0 would move the chosen unit onto the sample and end
+    # the tie, so every step is taken from the same state
+    for t in range(32):
+        _, f_wide = oracle.train_near_tie(W0, 1, 2, X, order[t:t + 1], s, 2e-7, 7, step0=t,
+                                          total_steps=32)
+        _, f_narrow = oracle.train_near_tie(W0, 1, 2, X, order[t:t + 1], s, 1e-8, 7,
+                                            step0=t, total_steps=32)
+        assert f_wide == int(bits[t]) and f_narrow == 0
+
+
 def test_argument_errors():
     X = np.zeros((2, 3), dtype=np.float32)
     W = np.zeros((4, 3))
     with pytest.raises(ValueError):
         oracle.train(W, 2, 2, X, np.array([5]), sched(0.1, 1.0))
+    with pytest.raises(ValueError):
+        oracle.train_near_tie(W, 2, 2, X, np.array([0]), sched(0.1, 1.0), -1.0, 0)
+    with pytest.raises(ValueError):
+        oracle.train_near_tie(W, 2, 2, X, np.array([0]), sched(0.1, 1.0), float("nan"), 0)
 
 
 # ------------------------------------------------------------ linear init (Sec. 6D, Fig. 2)
