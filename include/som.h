@@ -209,6 +209,26 @@ som_status som_bmu(som_map *map, const float *X, int64_t n, int32_t *out_idx);
 som_status som_bmu2(som_map *map, const float *X, int64_t n, int32_t *out_idx,
                     int32_t *out_idx2, float *out_d1);
 
+/* As som_bmu2, for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same kernels and the same outputs, but no hipMalloc, hipFree or
+ * allocating library routine is called.  The call's scratch (the
+ * prototypes' squared norms, the candidate lists, and the BMUs when
+ * out_idx is NULL) lives in one fixed 8 MiB array per device, held from
+ * the library's load until the process ends; it needs
+ *     roundup256(4 N) + roundup256(16 n G) + (out_idx ? 0 : roundup256(4 n))
+ * bytes (N units, G the unit groups of the candidate search: 1 when
+ * n >= 32705, at most roundup(N, 128) / 128 below), and a call whose
+ * inputs need more returns SOM_E_UNSUPPORTED without launching anything.
+ * Every call on a device shares that device's array and overwrites what
+ * it needs before reading it, so calls that overlap on one device (on
+ * different streams, or from different host threads) race; order them.
+ * The map's device must be the current device.  Stream-ordered.
+ * Errors: as som_bmu2, and SOM_E_ARG (the map's device is not current),
+ * SOM_E_UNSUPPORTED (scratch beyond the fixed array). */
+som_status som_bmu2_noalloc(som_map *map, const float *X, int64_t n, int32_t *out_idx,
+                            int32_t *out_idx2, float *out_d1);
+
 /* Quantization error (Sec. 6D, Sec. 8B): mean over the n samples of the
  * unsquared Euclidean distance to the BMU, accumulated in fp64.  *out_qe is
  * a host double.  Synchronizes the stream. */

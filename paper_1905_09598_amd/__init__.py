@@ -28,7 +28,7 @@ __all__ = [
     "som_quantization_error", "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
     "som_pca2", "som_suggest_size", "som_init_linear", "som_evaluate", "som_stream_inplace",
-    "som_status_string", "RECT", "HEX", "LINEAR", "EXPONENTIAL", "EXPORTED",
+    "som_bmu2_noalloc", "som_status_string", "RECT", "HEX", "LINEAR", "EXPONENTIAL", "EXPORTED",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -48,7 +48,7 @@ EXPORTED = (
     "som_topographic_error", "som_get_weights", "som_set_weights",
     "som_synchronize", "som_get_shape", "som_shuffle", "som_train_plan",
     "som_pca2", "som_suggest_size", "som_init_linear", "som_evaluate", "som_stream_inplace",
-    "som_status_string",
+    "som_bmu2_noalloc", "som_status_string",
 )
 
 
@@ -101,6 +101,7 @@ def lib():
         "som_train_batch": [vp, vp, i64, i32, C.c_double, C.c_double, i32],
         "som_bmu": [vp, vp, i64, vp],
         "som_bmu2": [vp, vp, i64, vp, vp, vp],
+        "som_bmu2_noalloc": [vp, vp, i64, vp, vp, vp],
         "som_quantization_error": [vp, vp, i64, C.POINTER(C.c_double)],
         "som_topographic_error": [vp, vp, i64, C.POINTER(C.c_double)],
         "som_get_weights": [vp, vp],
@@ -208,6 +209,11 @@ def som_bmu(handle: int, X, n: int, out_idx) -> None:
 def som_bmu2(handle: int, X, n: int, out_idx, out_idx2=None, out_d1=None) -> None:
     _check(lib().som_bmu2(handle, _ptr(X), n, _ptr(out_idx), _ptr(out_idx2),
                           _ptr(out_d1)), "som_bmu2")
+
+
+def som_bmu2_noalloc(handle: int, X, n: int, out_idx, out_idx2=None, out_d1=None) -> None:
+    _check(lib().som_bmu2_noalloc(handle, _ptr(X), n, _ptr(out_idx), _ptr(out_idx2),
+                                  _ptr(out_d1)), "som_bmu2_noalloc")
 
 
 def som_quantization_error(handle: int, X, n: int) -> float:

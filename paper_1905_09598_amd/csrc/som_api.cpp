@@ -768,6 +768,50 @@ som_status som_bmu2(som_map *m, const float *X, int64_t n, int32_t *out_idx,
     return run_eval(m, X, n, out_idx ? out_idx : m->idx1, out_idx2, out_d1);
 }
 
+som_status som_bmu2_noalloc(som_map *m, const float *X, int64_t n, int32_t *out_idx,
+                            int32_t *out_idx2, float *out_d1) {
+    if (!eval_args_ok(m, X, n)) return SOM_E_ARG;
+    if (out_idx && !device_range_ok(out_idx, (uint64_t)n * 4)) return SOM_E_ARG;
+    if (out_idx2 && !device_range_ok(out_idx2, (uint64_t)n * 4)) return SOM_E_ARG;
+    if (out_d1 && !device_range_ok(out_d1, (uint64_t)n * 4)) return SOM_E_ARG;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return from_hip(e);
+    if (dev != m->device) return SOM_E_ARG;
+    som::EvalArgs a{};
+    a.W = m->W;
+    a.ld = m->ld;
+    a.N = m->N;
+    a.d = m->d;
+    a.rows = m->rows;
+    a.cols = m->cols;
+    a.topology = m->topology;
+    a.X = X;
+    a.n = n;
+    som::plan_bmu_candidates(&a);
+    // scratch layout: prototype norms | candidates | BMUs when out_idx is NULL
+    const auto round256 = [](uint64_t b) { return (b + 255) / 256 * 256; };
+    const uint64_t norm_bytes = round256((uint64_t)m->N * 4);
+    const uint64_t cand_bytes = round256((uint64_t)n * (uint64_t)a.ugroups * som::kCand * 4);
+    const uint64_t idx_bytes = out_idx ? 0 : round256((uint64_t)n * 4);
+    if (norm_bytes + cand_bytes + idx_bytes > som::kNoAllocScratchBytes) return SOM_E_UNSUPPORTED;
+    void *base = nullptr;
+    e = som::noalloc_scratch(&base);
+    if (e != hipSuccess) return from_hip(e);
+    unsigned char *p = static_cast<unsigned char *>(base);
+    float *wnorm = reinterpret_cast<float *>(p);
+    a.wnorm = wnorm;
+    a.cand = reinterpret_cast<int32_t *>(p + norm_bytes);
+    a.idx1 = out_idx ? out_idx : reinterpret_cast<int32_t *>(p + norm_bytes + cand_bytes);
+    a.idx2 = out_idx2;
+    a.d1 = out_d1;
+    a.x_vec4 = (m->d % 4 == 0) && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
+    e = som::launch_row_sqnorm(m->W, m->ld, m->N, wnorm, m->stream);
+    if (e == hipSuccess) e = som::launch_bmu_candidates(a, m->stream);
+    if (e == hipSuccess) e = som::launch_bmu_rerank(a, m->stream);
+    return from_hip(e);
+}
+
 som_status som_bmu(som_map *m, const float *X, int64_t n, int32_t *out_idx) {
     if (!out_idx) return SOM_E_ARG;
     return som_bmu2(m, X, n, out_idx, nullptr, nullptr);

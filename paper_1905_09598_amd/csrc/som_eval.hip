@@ -17,6 +17,8 @@
 
 #include <math.h>
 
+#include <mutex>
+
 namespace som {
 namespace {
 
@@ -285,6 +287,33 @@ __global__ __launch_bounds__(kReduceBlock) void qe_te_reduce_kernel(
 }
 
 }  // namespace
+
+// Scratch of the evaluation entry point that allocates nothing
+// (som_bmu2_noalloc): one fixed array per device, held from the code
+// object's load until the process ends.  Host code never passes the array's
+// name to a kernel: it is a host-side stand-in, not a device address; the
+// address each device holds it at comes from hipGetSymbolAddress below.
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+hipError_t noalloc_scratch(void **ptr) {
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
 
 void plan_bmu_candidates(EvalArgs *a) {
     const int64_t tiles = (a->n + kBM - 1) / kBM;

@@ -131,6 +131,10 @@ constexpr int kCand = 4;
 // chip when n is small (sets a->ugroups and a->group_units).
 void plan_bmu_candidates(EvalArgs *a);
 hipError_t launch_bmu_candidates(const EvalArgs &a, hipStream_t s);
+// Fixed per-device scratch of som_bmu2_noalloc (som_eval.hip): its device
+// address on the current device, looked up once per device.
+constexpr size_t kNoAllocScratchBytes = 8u << 20;
+hipError_t noalloc_scratch(void **ptr);
 hipError_t launch_bmu_rerank(const EvalArgs &a, hipStream_t s);
 // QE and TE sums over n samples from (idx1, idx2, d1); writes 2 doubles.
 hipError_t launch_qe_te_reduce(const int32_t *idx1, const int32_t *idx2,
