@@ -278,6 +278,10 @@ def main():
                          "divides N / G), the same samples, d and schedule; the arg-min "
                          "exchange between GPUs is not built, so this is the per-GPU "
                          "kernel at its real shape")
+    ap.add_argument("--stream-sweep", action="store_true",
+                    help="instead of the bench line: the in-place stream's rate over buffers "
+                         "of 8 MB ... 4 GB on 256 and 1024 workgroups (one JSON line each), "
+                         "which shows where the memory side stops caching the footprint")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (the "
                          "reference dispatch for scaling HBM byte counters) and exit")
@@ -293,6 +297,14 @@ def main():
         return
     if args.map_sweep:
         map_sweep(args.cpu_budget)
+        return
+    if args.stream_sweep:
+        import torch
+        torch.cuda.set_device(0)
+        for mb in (8, 16, 32, 64, 82, 100, 128, 192, 256, 384, 512, 1024, 4096):
+            for grid in (256, 1024):
+                r = stream_inplace(mb * 1000 * 1000, grid)
+                print(json.dumps({"stream_inplace_MB": mb, **r}), flush=True)
         return
     if args.batch_map:
         batch_map_epoch(args.workload, args.steps, args.warmup)
