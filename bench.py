@@ -196,7 +196,8 @@ def map_sweep(cpu_budget: float):
         line = {"map": f"{side}x{side}", "units": N, "d": d, "steps": n,
                 "us_per_step": t / n * 1e6, "proto_dim_updates_per_s": n * N * d / t,
                 "train_s": t, "grid": plan["grid"],
-                "variant": ["stream", "lds", "pipelined-stream", "pipelined-lds"][plan["variant"]]}
+                "variant": ["stream", "lds", "pipelined-stream", "pipelined-lds",
+                            "pipelined-stream-cols"][plan["variant"]]}
         if cpu_budget > 0:
             W = oracle.init_uniform(0, N, d)
             s_ = oracle.schedule(0.5, 0.01, side / 2.0, 1.0)
@@ -451,12 +452,14 @@ def measure(cfg, input_kind: str, steps: int, warmup: int):
     achieved = alg_bytes / avg_train_s / 1e9
     traffic = measured_traffic(cfg.name)
     kernel_name = ["train_kernel (stream)", "train_kernel (lds)",
-                   "train_pipe_kernel (stream)", "train_pipe_kernel (lds)"][plan["variant"]]
-    variant = ["stream", "lds", "pipelined-stream", "pipelined-lds"][plan["variant"]]
+                   "train_pipe_kernel (stream)", "train_pipe_kernel (lds)",
+                   "train_pipe_kernel (stream, column walk)"][plan["variant"]]
+    variant = ["stream", "lds", "pipelined-stream", "pipelined-lds",
+               "pipelined-stream-cols"][plan["variant"]]
     grid, block = plan["grid"], plan["block"]
     # the LDS-resident kernels keep W on chip and wait on the grid exchange;
     # the streamed ones read and write W once per block of steps
-    bound = "hbm" if plan["variant"] in (0, 2) else "latency"
+    bound = "hbm" if plan["variant"] in (0, 2, 4) else "latency"
     if sparse:
         # the sparse path's own bytes: the dense 3 N d 4 per step does not
         # describe a kernel that touches only the sample's features

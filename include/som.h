@@ -131,7 +131,10 @@ som_status som_set_stream(som_map *map, void *stream);
  * row-major fp32 device matrix X, as one persistent cooperative kernel that
  * keeps the whole per-sample loop on the device.  Stream-ordered.  When d is
  * not a multiple of 4 or X is not 16-byte aligned, X is first copied into a
- * buffer of n * roundup(d, 4) floats that the map keeps for later calls.
+ * buffer of n * roundup(d, 4) floats that the map keeps for later calls;
+ * when the plan is the long-row kernel (som_train_plan variant 4) and the
+ * prototypes' row pitch exceeds d, into a buffer of n rows of that pitch
+ * (zero past d).
  * Errors: SOM_E_ARG (map, X or sched NULL, n <= 0, epochs <= 0, epochs * n
  * beyond 2^31 - 1, bad decay kind, lr < 0 or not finite, sigma < 0 or NaN,
  * exponential decay with a zero or infinite endpoint, total_steps too small,
@@ -313,7 +316,9 @@ som_status som_init_linear(som_map *map, const float *X, int64_t n);
  * per workgroup, kernel variant (0 = prototypes streamed from memory once
  * per block of steps, 1 = prototypes held in LDS for the whole call, 2 / 3 =
  * the same with the pass over the prototypes overlapped with the grid
- * exchanges) and steps per block (the number of consecutive samples whose
+ * exchanges, 4 = as 2 for rows too long to keep the samples' slices in
+ * registers: the pass walks the columns and loads each column slice of the
+ * samples once for all rows) and steps per block (the number of consecutive samples whose
  * updates one pass over the prototypes applies).  Any output may be NULL. */
 som_status som_train_plan(const som_map *map, int32_t *grid, int32_t *block,
                           int32_t *variant, int32_t *block_steps);

@@ -611,9 +611,11 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
         }
         a.block_dots = m->block_dots;
     }
-    if (m->d % 4 != 0 || reinterpret_cast<uintptr_t>(X) % 16 != 0) {
-        // The training kernels read sample rows as aligned float4.
-        const int64_t xld = ((int64_t)m->d + 3) & ~(int64_t)3;
+    // The training kernels read sample rows as aligned float4; the long-row
+    // kernel reads them as long as the prototypes' rows (zero past d).
+    const bool full_rows = plan.cols_rmax > 0 && m->ld != (int64_t)m->d;
+    if (m->d % 4 != 0 || reinterpret_cast<uintptr_t>(X) % 16 != 0 || full_rows) {
+        const int64_t xld = full_rows ? m->ld : ((int64_t)m->d + 3) & ~(int64_t)3;
         if (m->xpad_cap < n * xld) {
             e = hipStreamSynchronize(m->stream);
             if (e == hipSuccess && m->xpad) e = hipFree(m->xpad);

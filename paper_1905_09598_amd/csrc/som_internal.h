@@ -57,10 +57,13 @@ struct TrainArgs {
 struct TrainPlan {
     int32_t grid = 0;
     int32_t block = kTrainBlock;
-    int32_t variant = 0;     // 0 streamed, 1 LDS-resident, 2 / 3 pipelined streamed / LDS
+    int32_t variant = 0;     // 0 streamed, 1 LDS-resident, 2 / 3 pipelined streamed / LDS,
+                             // 4 pipelined streamed for long rows (column-walk sweep)
     int32_t block_m = 0;     // steps per block of the chosen kernel instance
     int32_t kslots = 0;      // float4 columns per lane (template instance)
     int32_t lds_rows = 0;    // pipelined streamed variant: rows per workgroup in LDS
+    int32_t cols_rmax = 0;   // pipelined streamed variant for long rows (column-walk
+                             // sweep): its row bound per workgroup, 0 otherwise
     int32_t slot_spread = 1;
     size_t lds_bytes = 0;
 };

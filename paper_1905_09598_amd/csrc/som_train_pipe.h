@@ -119,11 +119,16 @@ struct PipeLayout {
     float *dots;   // 2 parities x Rp rows x 3 sweepers x 2M
     float *coef;   // 2 parities x Rp x (M + 1)
     float4 *pos;   // Rp
+    f4 *dummy;     // column-walk sweep: 3 sweepers x 64 float4 that its
+                   // discarded LDS row writes land in
     f4 *lw;        // R x P4 (LDS variant)
 };
 
+// The column-walk sweep's discarded-write area, in float4.
+constexpr int kPipeDummy = kSweepers * 64;
+
 template <int M>
-__device__ inline PipeLayout pipe_layout(unsigned char *smem, int R) {
+__device__ inline PipeLayout pipe_layout(unsigned char *smem, int R, bool cols) {
     PipeLayout l;
     l.Rp = (R + 3) & ~3;
     unsigned char *p = smem + kPipeHeader;
@@ -134,6 +139,8 @@ __device__ inline PipeLayout pipe_layout(unsigned char *smem, int R) {
     p = reinterpret_cast<unsigned char *>((reinterpret_cast<uintptr_t>(p) + 15) & ~(uintptr_t)15);
     l.pos = reinterpret_cast<float4 *>(p);
     p += (size_t)l.Rp * 16;
+    l.dummy = reinterpret_cast<f4 *>(p);
+    if (cols) p += (size_t)kPipeDummy * 16;
     l.lw = reinterpret_cast<f4 *>(p);
     return l;
 }
@@ -308,6 +315,201 @@ __device__ inline void sweep_rows(f4 *lw, int RL, f4 *gs, int R, int P4, int nw,
                                                      dots + (size_t)RL * kSweepers * ND);
 }
 
+// ---------------------------------------------------------------- long rows
+// Sample indices of the M steps of block blk (steps past the end: sample 0).
+template <int M>
+__device__ inline void block_indices(int (&idx)[M], const TrainArgs &a, int64_t blk,
+                                     StepWindow<int> &ow) {
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+        const int64_t st = blk * M + j;
+        idx[j] = st < a.nsteps ? ow.get(a, st) : 0;
+    }
+}
+
+// The same pass as sweep_rows, for rows too long for three blocks of sample
+// slices to stay in registers: the sweeper walks its slices and, for each,
+// every row of the workgroup; the samples' rows must be as long as the
+// prototypes' (xld = ld, zero past d).  A slice of the 3 M samples (the previous
+// block's for the update, the current block's for the centring and the
+// current products, the next block's for the next products) is loaded from
+// memory once per slice and reused for all rows; the samples are read by
+// every workgroup, so they come from L2.  The products of each row
+// accumulate in registers across the slices (RMAX rows at most) and are
+// reduced over the lanes once, at the end.  Rows [0, RL) (RL <= RLMAX) live
+// in LDS, the others stream from memory at gs; the next slice's rows and
+// samples are loaded while the current one is computed.  Arguments as
+// sweep_rows; ip, ic, inx are the sample indices of the previous, current
+// and next block; dummy is this sweeper's 64-float4 area for the LDS writes
+// of streamed rows.
+template <int M, int RMAX, int RLMAX, bool MAT, bool ADOT, bool BDOT>
+__device__ inline void sweep_cols(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, int R, int P4,
+                                  int nw, const int (&ip)[M], const int (&ic)[M],
+                                  const int (&inx)[M], const float *coef_prev, float *dots,
+                                  f4 *dummy_p) {
+    constexpr int ND = 2 * M;
+    constexpr bool DOTS = ADOT || BDOT;
+    constexpr int NA = ND + 1;  // f.f, f.x_i, f.xn_j and f.z (last)
+    // The sweeper index and its slice count as scalars: left as functions
+    // of the thread index they would make the slice loop divergent, and
+    // every row offset with it.
+    const int s = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    nw = __builtin_amdgcn_readfirstlane(nw);
+    if (R <= 0 || nw <= 0) return;
+    row_t<true> *lw = rows_as<true>(lw_p);
+    row_t<true> *dummy = rows_as<true>(dummy_p);
+    const int lane = threadIdx.x & 63;
+    const int RS = R - RL;  // streamed rows
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        gs, (short)0, RS > 0 ? RS * P4 * 16 : 0, 0x00020000);
+    constexpr int kOutside = 1 << 30;  // bytes, beyond any sweep's rows
+    // Streamed row r's byte offset (a scalar per row): LDS rows and rows
+    // past R read zeros and drop their stores.
+    int soff[RMAX];
+#pragma unroll
+    for (int r = 0; r < RMAX; ++r)
+        soff[r] = __builtin_amdgcn_readfirstlane((r >= RL && r < R) ? (r - RL) * P4 * 16 : kOutside);
+    const auto row_off = [&](int r) { return soff[r]; };
+    float acc[RMAX][NA];
+#pragma unroll
+    for (int r = 0; r < RMAX; ++r)
+#pragma unroll
+        for (int t = 0; t < NA; ++t) acc[r][t] = 0.f;
+    // The rows' update coefficients, in registers for the whole pass: read
+    // from LDS per row and slice, each read's wait would also wait for the
+    // LDS rows in flight.
+    float cf[RMAX][M + 1];
+    if (MAT) {
+#pragma unroll
+        for (int r = 0; r < RMAX; ++r)
+#pragma unroll
+            for (int i = 0; i <= M; ++i) cf[r][i] = coef_prev[(r < R ? r : 0) * (M + 1) + i];
+    }
+    const float *xprev[M], *xcur[M], *xnext[M];
+#pragma unroll
+    for (int i = 0; i < M; ++i) {
+        xprev[i] = a.X + (int64_t)ip[i] * a.xld;
+        xcur[i] = a.X + (int64_t)ic[i] * a.xld;
+        xnext[i] = a.X + (int64_t)inx[i] * a.xld;
+    }
+    const auto slice_col = [&](int t) {
+        const int tc = t < nw ? t : nw - 1;  // clamped: its values go unused
+        return 64 * (s + kSweepers * tc) + lane;
+    };
+    // One slice's rows and samples.  The next slice's are all loaded at the
+    // start of the current one, ahead of its stores: the wait for a slice's
+    // loads then finds them issued a whole slice earlier (the memory counter
+    // is waited on in issue order, stores included).  Loads are
+    // unconditional: a select or branch on a value as it is loaded would
+    // make the compiler wait for it on the spot.
+    struct Slice {
+        f4 g[RMAX];   // streamed rows
+        f4 l[RLMAX];  // LDS rows
+        f4 x[3][M];   // samples: previous, current, next block
+    };
+    // (a 32-bit unsigned byte offset from a scalar row base: one address
+    // register per slice for all the samples)
+    const auto at = [](const float *row, unsigned off) {
+        return *(gf4 *)((const __attribute__((address_space(1))) char *)row + off);
+    };
+    const auto load = [&](int q, Slice &sl) {
+#pragma unroll
+        for (int r = 0; r < RMAX; ++r)
+            sl.g[r] = __builtin_bit_cast(
+                f4, __builtin_amdgcn_raw_buffer_load_b128(rs, q * 16, row_off(r), 0));
+        // (with no LDS rows this reads the slack after the layout, unused)
+        const int ql = RL > 0 ? q : lane;
+#pragma unroll
+        for (int r = 0; r < RLMAX; ++r) sl.l[r] = lw[(size_t)(r < RL ? r : 0) * P4 + ql];
+        const unsigned off = (unsigned)q * 16u;
+#pragma unroll
+        for (int i = 0; i < M; ++i) {
+            if (MAT) sl.x[0][i] = at(xprev[i], off);
+            if (DOTS && (i == 0 || ADOT)) sl.x[1][i] = at(xcur[i], off);
+            if (BDOT) sl.x[2][i] = at(xnext[i], off);
+        }
+    };
+    const auto work = [&](int t, Slice &sl) {
+        const int q = 64 * (s + kSweepers * t) + lane;
+        // Every row slot is computed, also past R (those read zeros and
+        // store nothing, and their sums are never read): a branch per row
+        // would merge the memory counters' state at each join, and the
+        // compiler would then wait for every load in flight.
+        // Streamed rows first and the LDS rows last: the memory counter's
+        // wait at the next slice then finds the last streamed store a few
+        // rows old.
+#pragma unroll
+        for (int rr = 0; rr < RMAX; ++rr) {
+            const int r = RMAX - 1 - rr;
+            f4 w = (r < RLMAX && r < RL) ? sl.l[r < RLMAX ? r : 0] : sl.g[r];
+            if (MAT) {
+                w = w * cf[r][0];
+#pragma unroll
+                for (int i = 0; i < M; ++i) {
+                    const float g = cf[r][1 + i];
+                    w.x = fmaf(g, sl.x[0][i].x, w.x);
+                    w.y = fmaf(g, sl.x[0][i].y, w.y);
+                    w.z = fmaf(g, sl.x[0][i].z, w.z);
+                    w.w = fmaf(g, sl.x[0][i].w, w.w);
+                }
+                if (r < RLMAX) {
+                    row_t<true> *dst = r < RL ? lw + (size_t)r * P4 + q : dummy + 64 * s + lane;
+                    *dst = w;
+                }
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, w), rs, q * 16,
+                                                       row_off(r), 0);
+            }
+            if (DOTS) {
+                const f4 z = sl.x[1][0];
+                const f4 f = w - z;
+                acc[r][0] = dot4(f, f, acc[r][0]);
+                acc[r][ND] = dot4(f, z, acc[r][ND]);
+                if (ADOT) {
+#pragma unroll
+                    for (int i = 1; i < M; ++i) acc[r][i] = dot4(f, sl.x[1][i], acc[r][i]);
+                }
+                if (BDOT) {
+#pragma unroll
+                    for (int j = 0; j < M; ++j) acc[r][M + j] = dot4(f, sl.x[2][j], acc[r][M + j]);
+                }
+            }
+        }
+    };
+    // Two slices per iteration, so that each buffer keeps its registers; an
+    // odd last slice is peeled.
+    Slice A, B;
+    load(slice_col(0), A);
+    int t = 0;
+    for (; t + 2 <= nw; t += 2) {
+        load(slice_col(t + 1), B);
+        work(t, A);
+        load(slice_col(t + 2), A);
+        work(t + 1, B);
+    }
+    if (t < nw) work(t, A);
+    if (DOTS) {
+        constexpr int NT = (NA + 3) / 4;
+#pragma unroll
+        for (int r = 0; r < RMAX; ++r) {
+            if (r < R) {
+                float tot[NT];
+                wave_sums_rows<NA>(acc[r], tot);
+                const float fz = lane_f(tot[ND / 4], 16 * sum_row(ND));
+                if ((lane & 15) == 0) {
+                    float *dr = dots + (r * kSweepers + s) * ND;
+                    const int qq = lane >> 4;
+#pragma unroll
+                    for (int j = 0; j < NT; ++j) {
+                        const int t = 4 * j + 2 * (qq & 1) + (qq >> 1);  // sum_row(t) == qq
+                        const bool used = t == 0 || (t < M ? ADOT : BDOT);
+                        if (t < ND) dr[t] = t == 0 ? tot[j] : (used ? tot[j] - fz : 0.f);
+                    }
+                }
+            }
+        }
+    }
+}
+
 // ---------------------------------------------------------------- controller
 // Controller lane r (< R): Gram matrix E of the next block from the sweep's
 // products of row r (d: f.f, f.A_1.., f.B_0.., summed over the sweepers),
@@ -365,7 +567,12 @@ struct SampleDots {
     __device__ float at(int t) const { return lane_f(v[t / 64], t % 64); }
 };
 
-template <int M, int KS, bool LDSW>
+// RMAX > 0: rows too long for sample registers, swept by sweep_cols (rows
+// streamed, at most RMAX per workgroup, the first RL <= kColsLdsRows of them
+// in LDS); KS is then unused.
+constexpr int kColsLdsRows = 4;
+
+template <int M, int KS, bool LDSW, int RMAX = 0>
 __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
     constexpr int T = M * (M + 1) / 2;
     constexpr int ND = 2 * M;
@@ -376,13 +583,13 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
     const int r1 = (int)(((int64_t)(b + 1) * a.N) / G);
     const int R = r1 - r0;  // 1 <= R <= 64 (planner)
     const int P4 = (int)(a.ld / 4);
-    const int nw = sweeper_slices(P4 / 64);  // <= KS (planner)
+    const int nw = sweeper_slices(P4 / 64);  // <= KS (planner) unless RMAX > 0
     const float inv_cols = 1.f / (float)a.cols;
     // Polls in flight per exchange: the LDS-resident kernels keep four; the
     // streamed ones one, where more polling traffic slows the row streams.
     constexpr int kPolls = LDSW ? 4 : 1;
     Bcast *bc = reinterpret_cast<Bcast *>(smem);
-    const PipeLayout l = pipe_layout<M>(smem, R);
+    const PipeLayout l = pipe_layout<M>(smem, R, RMAX > 0);
 
     if (a.state->order_bad) return;  // same value for every workgroup
     if (a.nsteps <= 0) return;
@@ -395,7 +602,8 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
     f4 *gw = reinterpret_cast<f4 *>(a.W) + (int64_t)r0 * P4;
     // Rows [0, RL) live in LDS for the whole launch; the streamed variant
     // keeps as many as its LDS holds (planner) and streams the rest.
-    const int RL = LDSW ? R : (a.lds_rows < R ? (a.lds_rows > 0 ? a.lds_rows : 0) : R);
+    int RL = LDSW ? R : (a.lds_rows < R ? (a.lds_rows > 0 ? a.lds_rows : 0) : R);
+    if (RMAX > 0 && RL > kColsLdsRows) RL = kColsLdsRows;
     if (RL > 0) {
         row_t<true> *lw = rows_as<true>(l.lw);
         const row_t<false> *g = rows_as<false>(gw);
@@ -471,6 +679,50 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
             __syncthreads();
             if (!ok) return;  // the sweepers read it from bc->abort
         }
+    } else if constexpr (RMAX > 0) {
+        // Long rows: the same block loop as below, with the samples' indices
+        // in place of their slices (sweep_cols loads the slices).
+        StepWindow<int> own;
+        own.init(a, 0);
+        int ip[M], ic[M], inx[M];
+        block_indices<M>(ic, a, 0, own);
+#pragma unroll
+        for (int j = 0; j < M; ++j) inx[j] = ip[j] = ic[j];
+        if (nb > 1) block_indices<M>(inx, a, 1, own);
+        f4 *dm = l.dummy;
+        sweep_cols<M, RMAX, kColsLdsRows, false, true, false>(
+            a, l.lw, RL, gs, R, P4, nw, ic, ic, ic, l.coef, l.dots + (size_t)l.Rp * kSweepers * ND,
+            dm);
+        __syncthreads();
+        for (int64_t blk = 0; blk < nb; ++blk) {
+            const int par = (int)(blk & 1);
+            const float *cp = l.coef + (size_t)(par ^ 1) * l.Rp * (M + 1);
+            float *dd = l.dots + (size_t)par * l.Rp * kSweepers * ND;
+            const bool has_next = blk + 1 < nb;
+            if (blk == 0) {
+                if (has_next)
+                    sweep_cols<M, RMAX, kColsLdsRows, false, true, true>(a, l.lw, RL, gs, R, P4, nw,
+                                                                         ip, ic, inx, cp, dd, dm);
+            } else if (has_next) {
+                sweep_cols<M, RMAX, kColsLdsRows, true, true, true>(a, l.lw, RL, gs, R, P4, nw, ip,
+                                                                    ic, inx, cp, dd, dm);
+            } else {
+                sweep_cols<M, RMAX, kColsLdsRows, true, false, false>(a, l.lw, RL, gs, R, P4, nw,
+                                                                      ip, ic, inx, cp, dd, dm);
+            }
+#pragma unroll
+            for (int j = 0; j < M; ++j) {
+                ip[j] = ic[j];
+                ic[j] = inx[j];
+            }
+            if (blk + 2 < nb) block_indices<M>(inx, a, blk + 2, own);
+            __syncthreads();
+            if (bc->abort) return;
+        }
+        // apply the last block's updates
+        sweep_cols<M, RMAX, kColsLdsRows, true, false, false>(
+            a, l.lw, RL, gs, R, P4, nw, ip, ic, inx,
+            l.coef + (size_t)((nb - 1) & 1) * l.Rp * (M + 1), l.dots, dm);
     } else {
         StepWindow<int> own;
         own.init(a, 0);
@@ -526,5 +778,8 @@ typedef void (*PipeKernel)(TrainArgs);
 // The streamed-prototype kernel for block length m and kslots ks, or null
 // when there is none (defined in som_train_pipe_stream.hip).
 PipeKernel pipe_stream_kernel(int m, int ks);
+// The long-row (column-walk) kernel for block length m and at most rmax
+// rows per workgroup, or null (som_train_pipe_stream.hip).
+PipeKernel pipe_cols_kernel(int m, int rmax);
 
 }  // namespace som

@@ -42,14 +42,24 @@ const PipeInstance *pipe_for(int m, int ks) {
     return nullptr;
 }
 
-size_t pipe_lds_bytes(int m, int rmax, int64_t P4, bool ldsw) {
+size_t pipe_lds_bytes(int m, int rmax, int64_t P4, bool ldsw, bool cols = false) {
     const size_t rp = (size_t)((rmax + 3) & ~3);
     size_t b = kPipeHeader + 2 * rp * kSweepers * 2 * m * 4 + 2 * rp * (m + 1) * 4;
     b = (b + 15) & ~(size_t)15;
     b += rp * 16;
+    // the column-walk sweep's discarded-write area, and 1 KB after the rows
+    // that its LDS row loads read when it holds no rows in LDS
+    if (cols) b += (size_t)kPipeDummy * 16 + 1024;
     if (ldsw) b += (size_t)rmax * P4 * 16;
     return b;
 }
+
+// Long-row (column-walk) instances: block length and row bound per
+// workgroup (som_train_pipe_stream.hip).
+struct ColsInstance {
+    int m, rmax;
+};
+const ColsInstance kCols[] = {{4, 10}};
 
 // Measured exchange latency of the pipelined kernel (multi-poll, per-XCD
 // replicated slots) by grid size, in microseconds.
@@ -123,6 +133,62 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
             }
         }
     }
+    // Rows too long for any instance above (their sample slices would not
+    // fit in registers): the column-walk sweep, rows streamed with the first
+    // few kept in LDS, when the workgroups own few enough rows.  Cost:
+    // about 0.128 us per row and slice of 64 float4 per sweeper (15 VALU
+    // operations per element and block, and the loop's overhead), 0.07 us
+    // per row for the lane sums, 0.5 us of hand-over per block, and at least
+    // the streamed rows' read and write at the workgroup's share of 6.8 TB/s
+    // (the in-place stream rate of a MALL-resident footprint); the
+    // controller as above.
+    const bool no_rows_instance = best >= 1e300;
+    for (const ColsInstance &ci : kCols) {
+        if (!no_rows_instance || a.variant == 1) break;
+        if (a.block_m > 0 && ci.m != a.block_m) continue;
+        for (int g = 1;; g = (g * 2 > max_grid && g < max_grid) ? max_grid : g * 2) {
+            const int gg = a.grid > 0 ? (a.grid < a.N ? a.grid : a.N) : g;
+            const int rmax = (a.N + gg - 1) / gg;
+            const size_t base = pipe_lds_bytes(ci.m, rmax, P4, false, true);
+            if (rmax <= ci.rmax && base <= (size_t)max_lds) {
+                int64_t fit = ((int64_t)max_lds - (int64_t)base) / (P4 * 16);
+                if (fit > kColsLdsRows) fit = kColsLdsRows;
+                int rl = (int)(fit < rmax ? fit : rmax);
+                if (a.lds_rows >= 0) rl = a.lds_rows < rl ? a.lds_rows : rl;
+                const double blk_us = rmax * (ks_need * 0.128 + 0.07) + 0.5;
+                const double mem_us = (rmax - rl) * P4 * 32.0 / (6.8e6 / gg);
+                const double sweep = (blk_us > mem_us ? blk_us : mem_us) / ci.m;
+                const double ctl = pipe_exchange_us(gg) + 0.03 * ci.m + 0.36 / ci.m;
+                const double t = sweep > ctl ? sweep : ctl;
+                if (t < best) {
+                    best = t;
+                    plan->grid = gg;
+                    plan->variant = 4;
+                    plan->block_m = ci.m;
+                    plan->kslots = 0;
+                    plan->lds_rows = rl;
+                    plan->cols_rmax = ci.rmax;
+                }
+            }
+            if (a.grid > 0 || g >= max_grid) break;
+        }
+    }
+    if (best < 1e300 && plan->cols_rmax > 0) {
+        plan->lds_bytes = pipe_lds_bytes(plan->block_m, (a.N + plan->grid - 1) / plan->grid, P4,
+                                          false, true) +
+                          (size_t)plan->lds_rows * P4 * 16;
+        if (plan->lds_bytes < 84 * 1024) plan->lds_bytes = 84 * 1024;
+        plan->block = 256;
+        plan->slot_spread = plan->grid <= 64 ? 16 : 4;
+        PipeKernel fn = pipe_cols_kernel(plan->block_m, plan->cols_rmax);
+        int per_cu = 0;
+        if (!fn ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &per_cu, reinterpret_cast<const void *>(fn), 256, plan->lds_bytes) != hipSuccess ||
+            per_cu < 1 || plan->grid > per_cu * num_cus || plan->grid > kMaxTrainGrid)
+            return 1e300;
+        return best;
+    }
     if (best < 1e300) {
         plan->lds_bytes = pipe_lds_bytes(plan->block_m, (a.N + plan->grid - 1) / plan->grid, P4,
                                           plan->variant == 3) +
@@ -152,9 +218,31 @@ int64_t pipe_block_dots_floats(int m, int64_t nsteps) {
 }
 
 hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStream_t s) {
+    const int64_t P4 = a.ld / 4;
+    if (plan.cols_rmax > 0) {
+        // long rows: the column-walk sweep (its prepass is the same)
+        PipeKernel fn = pipe_cols_kernel(plan.block_m, plan.cols_rmax);
+        DotsKernel dots = nullptr;
+        for (const PipeInstance &p : kPipe)
+            if (p.m == plan.block_m) dots = p.dots;
+        if (!fn || !dots || !a.block_dots || P4 % 64 != 0 || a.xld != a.ld ||
+            (a.N + plan.grid - 1) / plan.grid > plan.cols_rmax || plan.variant != 4 ||
+            plan.lds_rows > kColsLdsRows)
+            return hipErrorInvalidValue;
+        TrainArgs args = a;
+        args.grid = plan.grid;
+        args.slot_spread = plan.slot_spread;
+        args.lds_rows = plan.lds_rows;
+        const int64_t nb = (a.nsteps + plan.block_m - 1) / plan.block_m;
+        dots<<<dim3((unsigned)nb), dim3(256), 0, s>>>(args, args.block_dots, nb);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        void *params[] = {&args};
+        return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),
+                                          dim3(256), params, (unsigned)plan.lds_bytes, s);
+    }
     const PipeInstance *pi = pipe_for(plan.block_m, plan.kslots);
     if (!pi || !a.block_dots) return hipErrorInvalidValue;
-    const int64_t P4 = a.ld / 4;
     if (P4 % 64 != 0 || (P4 / 64 + kSweepers - 1) / kSweepers != pi->ks ||
         (a.N + plan.grid - 1) / plan.grid > 64)
         return hipErrorInvalidValue;

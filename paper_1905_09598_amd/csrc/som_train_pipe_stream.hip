@@ -24,4 +24,17 @@ PipeKernel pipe_stream_kernel(int m, int ks) {
     return nullptr;
 }
 
+PipeKernel pipe_cols_kernel(int m, int rmax) {
+    struct Entry {
+        int m, rmax;
+        PipeKernel fn;
+    };
+    static const Entry kCols[] = {
+        {4, 10, train_pipe_kernel<4, 1, false, 10>},
+    };
+    for (const Entry &e : kCols)
+        if (e.m == m && e.rmax == rmax) return e.fn;
+    return nullptr;
+}
+
 }  // namespace som

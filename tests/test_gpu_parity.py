@@ -577,6 +577,50 @@ def test_large_maps_at_small_d_follow_the_oracle(side):
     _train_vs_oracle(side, side, 64, 150, 1)
 
 
+# Rows too long for the pipelined kernel's sample registers, on its
+# column-walk sweep (plan variant 4): ragged row counts per workgroup, slices
+# reaching past d (zeros there), sweepers with different slice counts, a
+# partial last block, and 0 to 4 rows kept in LDS.
+@pytest.mark.parametrize("rows,cols,d,n,epochs,grid", [
+    (5, 4, 6000, 31, 2, 3),      # 6-7 rows per workgroup, 24 slices (8 each)
+    (4, 4, 9500, 31, 2, 2),      # 8 rows, 40 slices (14 / 13 / 13), ragged tail slice
+    (3, 5, 12000, 25, 1, 2),     # 7-8 rows, 48 slices
+    (3, 3, 16000, 17, 2, 1),     # 9 rows on one workgroup, 64 slices
+    (4, 3, 7001, 20, 1, 2),      # d not a multiple of 4: padded sample copy
+    (10, 10, 6000, 23, 1, 10),   # 10 rows per workgroup, the kernel's bound
+])
+@pytest.mark.parametrize("lds_rows", ["0", "1", "4"])
+def test_long_rows_pipelined_follow_the_oracle(rows, cols, d, n, epochs, grid, lds_rows,
+                                               monkeypatch):
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", "4")
+    monkeypatch.setenv("SOM_TRAIN_GRID", str(grid))
+    monkeypatch.setenv("SOM_TRAIN_LDS_ROWS", lds_rows)
+    say("long rows", rows, cols, d, n, epochs, "grid", grid, "lds_rows", lds_rows)
+    plan = _train_vs_oracle(rows, cols, d, n, epochs)
+    assert plan["variant"] == 4 and plan["grid"] == grid
+
+
+def test_long_rows_pipelined_hexagonal_and_schedule_edges(monkeypatch):
+    # the column-walk sweep on a hexagonal lattice, then a unit rate with a
+    # zero radius, which must copy each sample exactly into its BMU
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", "4")
+    say("long rows hex")
+    plan = _train_vs_oracle(4, 5, 8000, 27, 2, topology=som.HEX)
+    assert plan["variant"] == 4
+    X = workloads.gaussian_mixture(9, 9000, 3, 0.2, seed=5)
+    W = workloads.random_weights(12, 9000, 6)
+    m = make_map(3, 4, 9000, W=W)
+    order = np.arange(9, dtype=np.int32)
+    trace = dev(np.full(9, -1, dtype=np.int32))
+    m.train(dev(X), 1, 1.0, 1.0, 0.0, 0.0, order=dev(order), bmu_trace=trace)
+    assert m.plan()["variant"] == 4
+    s = oracle.schedule(1.0, 1.0, 0.0, 0.0, oracle.LINEAR, oracle.LINEAR)
+    Wo, tr = oracle.train(W, 3, 4, X, order, s, trace=True)
+    assert np.array_equal(trace.cpu().numpy(), tr)
+    assert np.array_equal(m.weights.cpu().numpy().astype(np.float64), Wo)
+    m.close()
+
+
 # The launch shapes the planner picks for the five workloads, as measured
 # fastest on MI355X (grid sweeps and block lengths at each workload): a
 # change of cost model that moves one of them shows up here.
@@ -584,7 +628,7 @@ def test_large_maps_at_small_d_follow_the_oracle(side):
     (0, 3, 8, 4),      # 10x10, d = 500: pipelined, LDS rows
     (1, 3, 64, 4),     # 20x20, d = 2000
     (2, 3, 256, 2),    # 30x30, d = 5000
-    (3, 0, 256, 3),    # 50x50, d = 10000: blocked, streamed rows
+    (3, 4, 256, 4),    # 50x50, d = 10000: pipelined, column walk over streamed rows
     (4, 2, 256, 4),    # 100x100, d = 2048: pipelined, streamed rows
 ])
 def test_workload_launch_shapes(ci, variant, grid, block_steps, monkeypatch):
