@@ -392,6 +392,10 @@ static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
     const char *bm = getenv("SOM_TRAIN_BLOCK_M");
     a.block_m = (bm && *bm) ? atoi(bm) : 0;
     if (a.block_m < 0) a.block_m = 0;
+    // SOM_TRAIN_SWEEPERS: 3 or 4 sweeper waves in the pipelined kernel.
+    const char *sw = getenv("SOM_TRAIN_SWEEPERS");
+    a.sweepers = (sw && *sw) ? atoi(sw) : 0;
+    if (a.sweepers != 3 && a.sweepers != 4) a.sweepers = 0;
     a.timeout_ticks = 100000000ull * 20;  // 20 s at the 100 MHz reference clock
     return a;
 }

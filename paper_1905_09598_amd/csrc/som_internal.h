@@ -51,6 +51,7 @@ struct TrainArgs {
     int32_t lds_rows;       // pipelined streamed variant: leading rows of each
                             // workgroup kept in LDS (-1 = planner's choice)
     int32_t block_m;        // pipelined kernel: requested block length (0 = any)
+    int32_t sweepers;       // pipelined kernel: requested sweeper waves (0 = any, 3, 4)
     uint64_t timeout_ticks; // bound of one exchange wait, in 100 MHz ticks
 };
 

@@ -51,8 +51,10 @@ namespace {  // each translation unit emits only the instances it uses
 
 using namespace dev;
 
-constexpr int kSweepers = 3;    // waves 0..2 sweep
-constexpr int kController = 3;  // wave 3 runs the exchanges
+// Waves 0 .. NS-1 sweep and wave NS runs the exchanges.  NS = 3 puts each
+// wave on a SIMD of its own; NS = 4 (the streamed kernels of long
+// sweeps) puts every SIMD to sweeping and the controller beside sweeper 0.
+constexpr int kSweepers = 3;
 constexpr int kPipeHeader = 64;
 
 template <int M>
@@ -127,13 +129,13 @@ struct PipeLayout {
 // The column-walk sweep's discarded-write area, in float4.
 constexpr int kPipeDummy = kSweepers * 64;
 
-template <int M>
+template <int M, int NS = kSweepers>
 __device__ inline PipeLayout pipe_layout(unsigned char *smem, int R, bool cols) {
     PipeLayout l;
     l.Rp = (R + 3) & ~3;
     unsigned char *p = smem + kPipeHeader;
     l.dots = reinterpret_cast<float *>(p);
-    p += (size_t)2 * l.Rp * kSweepers * 2 * M * 4;
+    p += (size_t)2 * l.Rp * NS * 2 * M * 4;
     l.coef = reinterpret_cast<float *>(p);
     p += (size_t)2 * l.Rp * (M + 1) * 4;
     p = reinterpret_cast<unsigned char *>((reinterpret_cast<uintptr_t>(p) + 15) & ~(uintptr_t)15);
@@ -146,15 +148,16 @@ __device__ inline PipeLayout pipe_layout(unsigned char *smem, int R, bool cols) 
 }
 
 // ---------------------------------------------------------------- sweepers
-// Sweeper slices: wave s owns slices s + 3t, t < nw (nw <= KS).
+// Sweeper slices: wave s owns slices s + NS t, t < nw (nw <= KS).
+template <int NS = kSweepers>
 __device__ inline int sweeper_slices(int nsl) {
     const int s = threadIdx.x >> 6;
-    return nsl > s ? (nsl - s + kSweepers - 1) / kSweepers : 0;
+    return nsl > s ? (nsl - s + NS - 1) / NS : 0;
 }
 
 // This wave's slices of the M samples of block blk (steps past the end load
 // sample 0; columns past d, and slices t >= nw, are zero).
-template <int M, int KS>
+template <int M, int KS, int NS = kSweepers>
 __device__ inline void load_samples(f4 (&x)[M][KS], const TrainArgs &a, int64_t blk,
                                     StepWindow<int> &ow) {
     const int lane = threadIdx.x & 63, s = threadIdx.x >> 6;
@@ -163,7 +166,7 @@ __device__ inline void load_samples(f4 (&x)[M][KS], const TrainArgs &a, int64_t 
         const int64_t st = blk * M + j;
         const int i = st < a.nsteps ? ow.get(a, st) : 0;
 #pragma unroll
-        for (int t = 0; t < KS; ++t) x[j][t] = sample_f4(a, i, 64 * (s + kSweepers * t) + lane);
+        for (int t = 0; t < KS; ++t) x[j][t] = sample_f4(a, i, 64 * (s + NS * t) + lane);
     }
 }
 
@@ -179,7 +182,7 @@ __device__ inline float dot4(f4 a, f4 b, float acc) {
 // coefficients) are loaded D rows ahead, into a ring of registers indexed
 // statically.  Callers sweeping a part of the rows pass coef_prev and dots
 // advanced to its first row.
-template <int M, int KS, int D, bool LDSW, bool MAT, bool ADOT, bool BDOT>
+template <int M, int KS, int D, bool LDSW, bool MAT, bool ADOT, bool BDOT, int NS = kSweepers>
 __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&xp)[M][KS],
                                   const f4 (&xc)[M][KS], const f4 (&xn)[M][KS],
                                   const float *coef_prev, float *dots) {
@@ -198,7 +201,7 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
         __builtin_amdgcn_make_buffer_rsrc(rows_p, (short)0, LDSW ? 0 : R * P4 * 16, 0x00020000);
     constexpr int kOutside = 1 << 30;  // bytes, beyond any sweep's rows
     const auto slice_off = [&](int r, int t) {
-        return t < nw ? (r * P4 + 64 * (s + kSweepers * t) + lane) * 16 : kOutside;
+        return t < nw ? (r * P4 + 64 * (s + NS * t) + lane) * 16 : kOutside;
     };
     f4 ring[D][KS];
     float cring[D][M + 1];
@@ -212,7 +215,7 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
 #pragma unroll
         for (int t = 0; t < KS; ++t) {
             if constexpr (LDSW) {
-                const int q = 64 * (s + kSweepers * t) + lane;
+                const int q = 64 * (s + NS * t) + lane;
                 dst[t] = rows[(size_t)rr * P4 + (q < P4 ? q : P4 - 1)];
             } else {
                 dst[t] = __builtin_bit_cast(
@@ -251,7 +254,7 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
                                 w.w = fmaf(g, xp[i][t].w, w.w);
                             }
                             if constexpr (LDSW) {
-                                if (t < nw) rows[(size_t)r * P4 + 64 * (s + kSweepers * t) + lane] = w;
+                                if (t < nw) rows[(size_t)r * P4 + 64 * (s + NS * t) + lane] = w;
                             } else {
                                 __builtin_amdgcn_raw_buffer_store_b128(
                                     __builtin_bit_cast(u32x4, w), rs, slice_off(r, t), 0, 0);
@@ -285,7 +288,7 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
                     const float fz = lane_f(tot[ND / 4], 16 * sum_row(ND));
                     if ((lane & 15) == 0) {
                         // lane 16 q writes the values its row holds
-                        float *dr = dots + (r * kSweepers + s) * ND;
+                        float *dr = dots + (r * NS + s) * ND;
                         const int q = lane >> 4;
 #pragma unroll
                         for (int j = 0; j < NT; ++j) {
@@ -303,16 +306,16 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
 // A sweep over the workgroup's R rows: rows [0, RL) from LDS (loaded two
 // ahead) and, in the streamed variant (LDSW false), rows [RL, R) from
 // memory at gs (loaded four ahead).
-template <int M, int KS, bool LDSW, bool MAT, bool ADOT, bool BDOT>
+template <int M, int KS, bool LDSW, bool MAT, bool ADOT, bool BDOT, int NS = kSweepers>
 __device__ inline void sweep_rows(f4 *lw, int RL, f4 *gs, int R, int P4, int nw,
                                   const f4 (&xp)[M][KS], const f4 (&xc)[M][KS],
                                   const f4 (&xn)[M][KS], const float *coef_prev, float *dots) {
     constexpr int ND = 2 * M;
-    pipe_sweep<M, KS, 2, true, MAT, ADOT, BDOT>(lw, RL, P4, nw, xp, xc, xn, coef_prev, dots);
+    pipe_sweep<M, KS, 2, true, MAT, ADOT, BDOT, NS>(lw, RL, P4, nw, xp, xc, xn, coef_prev, dots);
     if constexpr (!LDSW)
-        pipe_sweep<M, KS, 4, false, MAT, ADOT, BDOT>(gs, R - RL, P4, nw, xp, xc, xn,
-                                                     coef_prev + (size_t)RL * (M + 1),
-                                                     dots + (size_t)RL * kSweepers * ND);
+        pipe_sweep<M, KS, 4, false, MAT, ADOT, BDOT, NS>(gs, R - RL, P4, nw, xp, xc, xn,
+                                                         coef_prev + (size_t)RL * (M + 1),
+                                                         dots + (size_t)RL * NS * ND);
 }
 
 // ---------------------------------------------------------------- long rows
@@ -572,8 +575,11 @@ struct SampleDots {
 // in LDS); KS is then unused.
 constexpr int kColsLdsRows = 4;
 
-template <int M, int KS, bool LDSW, int RMAX = 0>
-__global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
+template <int M, int KS, bool LDSW, int RMAX = 0, int NS = kSweepers>
+__global__ __launch_bounds__(64 * (NS + 1), 1) void train_pipe_kernel(TrainArgs a) {
+    static_assert(RMAX == 0 || NS == kSweepers, "the column-walk sweep runs three sweepers");
+    constexpr int kBlock = 64 * (NS + 1);
+    constexpr int kController = NS;
     constexpr int T = M * (M + 1) / 2;
     constexpr int ND = 2 * M;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -583,18 +589,18 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
     const int r1 = (int)(((int64_t)(b + 1) * a.N) / G);
     const int R = r1 - r0;  // 1 <= R <= 64 (planner)
     const int P4 = (int)(a.ld / 4);
-    const int nw = sweeper_slices(P4 / 64);  // <= KS (planner) unless RMAX > 0
+    const int nw = sweeper_slices<NS>(P4 / 64);  // <= KS (planner) unless RMAX > 0
     const float inv_cols = 1.f / (float)a.cols;
     // Polls in flight per exchange: the LDS-resident kernels keep four; the
     // streamed ones one, where more polling traffic slows the row streams.
     constexpr int kPolls = LDSW ? 4 : 1;
     Bcast *bc = reinterpret_cast<Bcast *>(smem);
-    const PipeLayout l = pipe_layout<M>(smem, R, RMAX > 0);
+    const PipeLayout l = pipe_layout<M, NS>(smem, R, RMAX > 0);
 
     if (a.state->order_bad) return;  // same value for every workgroup
     if (a.nsteps <= 0) return;
 
-    for (int r = tid; r < R; r += 256) {
+    for (int r = tid; r < R; r += kBlock) {
         const int u = r0 + r, ur = u / a.cols, uc = u - ur * a.cols;
         l.pos[r] = make_float4((float)ur, (float)uc, (float)(ur & 1), 0.f);
     }
@@ -607,7 +613,7 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
     if (RL > 0) {
         row_t<true> *lw = rows_as<true>(l.lw);
         const row_t<false> *g = rows_as<false>(gw);
-        for (int e = tid; e < RL * P4; e += 256) lw[e] = g[e];
+        for (int e = tid; e < RL * P4; e += kBlock) lw[e] = g[e];
     }
     f4 *gs = gw + (int64_t)RL * P4;  // first streamed row
     const int64_t nb = (a.nsteps + M - 1) / M;
@@ -642,9 +648,14 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
             const int par = (int)(blk & 1);
             float E[T], d[ND];
             const float *dr =
-                l.dots + ((size_t)(par ^ 1) * l.Rp + (lane < R ? lane : 0)) * kSweepers * ND;
+                l.dots + ((size_t)(par ^ 1) * l.Rp + (lane < R ? lane : 0)) * NS * ND;
 #pragma unroll
-            for (int t = 0; t < ND; ++t) d[t] = (dr[t] + dr[ND + t]) + dr[2 * ND + t];
+            for (int t = 0; t < ND; ++t) {
+                if constexpr (NS == 4)
+                    d[t] = (dr[t] + dr[ND + t]) + (dr[2 * ND + t] + dr[3 * ND + t]);
+                else
+                    d[t] = (dr[t] + dr[ND + t]) + dr[2 * ND + t];
+            }
             if (blk == 0) {
                 // the initial prototypes' products with block 0 itself:
                 // f.B_j = f.A_j (B_0 = A_0 = 0)
@@ -728,25 +739,28 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
         own.init(a, 0);
         // Slices of the samples of the previous, current and next block.
         f4 xp[M][KS], xc[M][KS], xn[M][KS];
-        load_samples<M, KS>(xc, a, 0, own);
-        if (nb > 1) load_samples<M, KS>(xn, a, 1, own);
+        load_samples<M, KS, NS>(xc, a, 0, own);
+        if (nb > 1) load_samples<M, KS, NS>(xn, a, 1, own);
         // Products of the initial prototypes with block 0 (centred on its
         // first sample): f.f and f.(x_{0,i} - z), parity 1.
-        sweep_rows<M, KS, LDSW, false, true, false>(l.lw, RL, gs, R, P4, nw, xc, xc, xc, l.coef,
-                                                 l.dots + (size_t)l.Rp * kSweepers * ND);
+        sweep_rows<M, KS, LDSW, false, true, false, NS>(l.lw, RL, gs, R, P4, nw, xc, xc, xc, l.coef,
+                                                     l.dots + (size_t)l.Rp * NS * ND);
         __syncthreads();
         for (int64_t blk = 0; blk < nb; ++blk) {
             const int par = (int)(blk & 1);
             const float *cp = l.coef + (size_t)(par ^ 1) * l.Rp * (M + 1);
-            float *dd = l.dots + (size_t)par * l.Rp * kSweepers * ND;
+            float *dd = l.dots + (size_t)par * l.Rp * NS * ND;
             const bool has_next = blk + 1 < nb;
             if (blk == 0) {
                 if (has_next)
-                    sweep_rows<M, KS, LDSW, false, true, true>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp, dd);
+                    sweep_rows<M, KS, LDSW, false, true, true, NS>(l.lw, RL, gs, R, P4, nw, xp, xc, xn,
+                                                                   cp, dd);
             } else if (has_next) {
-                sweep_rows<M, KS, LDSW, true, true, true>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp, dd);
+                sweep_rows<M, KS, LDSW, true, true, true, NS>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp,
+                                                              dd);
             } else {
-                sweep_rows<M, KS, LDSW, true, false, false>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp, dd);
+                sweep_rows<M, KS, LDSW, true, false, false, NS>(l.lw, RL, gs, R, P4, nw, xp, xc, xn,
+                                                                cp, dd);
             }
 #pragma unroll
             for (int j = 0; j < M; ++j)
@@ -755,12 +769,12 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
                     xp[j][t] = xc[j][t];
                     xc[j][t] = xn[j][t];
                 }
-            if (blk + 2 < nb) load_samples<M, KS>(xn, a, blk + 2, own);
+            if (blk + 2 < nb) load_samples<M, KS, NS>(xn, a, blk + 2, own);
             __syncthreads();
             if (bc->abort) return;
         }
         // apply the last block's updates
-        sweep_rows<M, KS, LDSW, true, false, false>(
+        sweep_rows<M, KS, LDSW, true, false, false, NS>(
             l.lw, RL, gs, R, P4, nw, xp, xc, xn, l.coef + (size_t)((nb - 1) & 1) * l.Rp * (M + 1),
             l.dots);
     }
@@ -768,16 +782,16 @@ __global__ __launch_bounds__(256, 1) void train_pipe_kernel(TrainArgs a) {
         __syncthreads();
         const row_t<true> *lw = rows_as<true>(l.lw);
         row_t<false> *g = rows_as<false>(gw);
-        for (int e = tid; e < RL * P4; e += 256) g[e] = lw[e];
+        for (int e = tid; e < RL * P4; e += kBlock) g[e] = lw[e];
     }
 }
 }  // namespace
 
 typedef void (*PipeKernel)(TrainArgs);
 
-// The streamed-prototype kernel for block length m and kslots ks, or null
-// when there is none (defined in som_train_pipe_stream.hip).
-PipeKernel pipe_stream_kernel(int m, int ks);
+// The streamed-prototype kernel for block length m, kslots ks and ns
+// sweepers, or null when there is none (defined in som_train_pipe_stream.hip).
+PipeKernel pipe_stream_kernel(int m, int ks, int ns);
 // The long-row (column-walk) kernel for block length m and at most rmax
 // rows per workgroup, or null (som_train_pipe_stream.hip).
 PipeKernel pipe_cols_kernel(int m, int rmax);

@@ -42,9 +42,10 @@ const PipeInstance *pipe_for(int m, int ks) {
     return nullptr;
 }
 
-size_t pipe_lds_bytes(int m, int rmax, int64_t P4, bool ldsw, bool cols = false) {
+size_t pipe_lds_bytes(int m, int rmax, int64_t P4, bool ldsw, bool cols = false,
+                      int ns = kSweepers) {
     const size_t rp = (size_t)((rmax + 3) & ~3);
-    size_t b = kPipeHeader + 2 * rp * kSweepers * 2 * m * 4 + 2 * rp * (m + 1) * 4;
+    size_t b = kPipeHeader + 2 * rp * ns * 2 * m * 4 + 2 * rp * (m + 1) * 4;
     b = (b + 15) & ~(size_t)15;
     b += rp * 16;
     // the column-walk sweep's discarded-write area, and 1 KB after the rows
@@ -60,6 +61,14 @@ struct ColsInstance {
     int m, rmax;
 };
 const ColsInstance kCols[] = {{4, 10}};
+
+// Streamed instances on four sweepers (block length, slices per sweeper):
+// every SIMD sweeps, the controller shares the first one
+// (som_train_pipe_stream.hip).
+struct Wide {
+    int m, ks;
+};
+const Wide kWide[] = {{4, 2}};
 
 // Measured exchange latency of the pipelined kernel (multi-poll, per-XCD
 // replicated slots) by grid size, in microseconds.
@@ -85,7 +94,7 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
     const int max_grid = a.N < num_cus ? a.N : num_cus;
     double best = 1e300;
     for (const PipeInstance &pi : kPipe) {
-        if (pi.ks != ks_need || (a.block_m > 0 && pi.m != a.block_m)) continue;
+        if (pi.ks != ks_need || (a.block_m > 0 && pi.m != a.block_m) || a.sweepers == 4) continue;
         for (int v = 0; v < 2; ++v) {
             const bool ldsw = v == 0;  // LDS first: it wins ties
             if ((a.variant == 1 && !ldsw) || (a.variant == 2 && ldsw)) continue;
@@ -127,10 +136,51 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                         plan->block_m = pi.m;
                         plan->kslots = pi.ks;
                         plan->lds_rows = ldsw ? 0 : rl;
+                        plan->block = 256;
                     }
                 }
                 if (a.grid > 0 || g >= max_grid) break;
             }
+        }
+    }
+    // Four sweepers for the streamed rows: the same pass split over four
+    // waves instead of three, on every SIMD, the controller beside the
+    // first sweeper.  Cost as above with the four-sweeper slice count and
+    // the first sweeper's rows 12 % slower (the controller's issue slots
+    // on its SIMD).
+    for (const Wide &wi : kWide) {
+        const int ks4 = (nsl + 3) / 4;
+        if (wi.ks != ks4 || a.variant == 1 || a.sweepers == 3 ||
+            (a.block_m > 0 && wi.m != a.block_m))
+            continue;
+        for (int g = 1;; g = (g * 2 > max_grid && g < max_grid) ? max_grid : g * 2) {
+            const int gg = a.grid > 0 ? (a.grid < a.N ? a.grid : a.N) : g;
+            const int rmax = (a.N + gg - 1) / gg;
+            const size_t base = pipe_lds_bytes(wi.m, rmax, P4, false, false, 4);
+            int rl = 0;
+            if (base < (size_t)max_lds) {
+                const int64_t fit = ((int64_t)max_lds - (int64_t)base) / (P4 * 16);
+                rl = (int)(fit < rmax ? fit : rmax);
+                if (a.lds_rows >= 0) rl = a.lds_rows < rl ? a.lds_rows : rl;
+            }
+            if (rmax <= 64 && base <= (size_t)max_lds) {
+                const double row_us = 1.12 * (ks4 * (0.027 * wi.m + 0.0395) + 0.012 * wi.m + 0.0665);
+                const double blk_us = rmax * row_us + (rmax - rl) * 0.05 + 0.5 + 0.15 * wi.m;
+                const double mem_us = (rmax - rl) * P4 * 32.0 / (8e6 / gg);
+                const double sweep = (blk_us > mem_us ? blk_us : mem_us) / wi.m;
+                const double ctl = pipe_exchange_us(gg) + 0.03 * wi.m + 0.36 / wi.m;
+                const double t = sweep > ctl ? sweep : ctl;
+                if (t < best) {
+                    best = t;
+                    plan->grid = gg;
+                    plan->variant = 2;
+                    plan->block_m = wi.m;
+                    plan->kslots = wi.ks;
+                    plan->lds_rows = rl;
+                    plan->block = 320;
+                }
+            }
+            if (a.grid > 0 || g >= max_grid) break;
         }
     }
     // Rows too long for any instance above (their sample slices would not
@@ -168,6 +218,7 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                     plan->kslots = 0;
                     plan->lds_rows = rl;
                     plan->cols_rmax = ci.rmax;
+                    plan->block = 256;
                 }
             }
             if (a.grid > 0 || g >= max_grid) break;
@@ -190,22 +241,28 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
         return best;
     }
     if (best < 1e300) {
+        const int ns = plan->block / 64 - 1;
         plan->lds_bytes = pipe_lds_bytes(plan->block_m, (a.N + plan->grid - 1) / plan->grid, P4,
-                                          plan->variant == 3) +
+                                          plan->variant == 3, false, ns) +
                           (size_t)plan->lds_rows * P4 * 16;
         if (plan->lds_bytes < 84 * 1024) plan->lds_bytes = 84 * 1024;
-        plan->block = 256;
         // Measured on MI355X: the LDS-resident kernels' multi-poll exchanges
         // are fastest with packed slots, the streamed kernels' one-poll
         // exchanges with one slot per 128-byte line up to 64 workgroups and
         // 32-byte spacing beyond.
         plan->slot_spread = plan->variant == 3 ? 1 : (plan->grid <= 64 ? 16 : 4);
-        const PipeInstance *pi = pipe_for(plan->block_m, plan->kslots);
-        PipeKernel fn = plan->variant == 3 ? pi->lds : pipe_stream_kernel(pi->m, pi->ks);
+        PipeKernel fn = nullptr;
+        if (plan->variant == 3) {
+            const PipeInstance *pi = pipe_for(plan->block_m, plan->kslots);
+            fn = pi ? pi->lds : nullptr;
+        } else {
+            fn = pipe_stream_kernel(plan->block_m, plan->kslots, ns);
+        }
         int per_cu = 0;
         if (!fn ||
             hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                &per_cu, reinterpret_cast<const void *>(fn), 256, plan->lds_bytes) != hipSuccess ||
+                &per_cu, reinterpret_cast<const void *>(fn), plan->block, plan->lds_bytes) !=
+                hipSuccess ||
             per_cu < 1 || plan->grid > per_cu * num_cus || plan->grid > kMaxTrainGrid)
             return 1e300;
     }
@@ -241,24 +298,29 @@ hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStrea
         return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),
                                           dim3(256), params, (unsigned)plan.lds_bytes, s);
     }
+    const int ns = plan.block / 64 - 1;
+    if (ns != 3 && ns != 4) return hipErrorInvalidValue;
+    DotsKernel dots = nullptr;
+    for (const PipeInstance &p : kPipe)
+        if (p.m == plan.block_m) dots = p.dots;
     const PipeInstance *pi = pipe_for(plan.block_m, plan.kslots);
-    if (!pi || !a.block_dots) return hipErrorInvalidValue;
-    if (P4 % 64 != 0 || (P4 / 64 + kSweepers - 1) / kSweepers != pi->ks ||
+    PipeKernel fn = plan.variant == 3 ? (pi && ns == 3 ? pi->lds : nullptr)
+                                      : pipe_stream_kernel(plan.block_m, plan.kslots, ns);
+    if (!fn || !dots || !a.block_dots) return hipErrorInvalidValue;
+    if (P4 % 64 != 0 || (P4 / 64 + ns - 1) / ns != plan.kslots ||
         (a.N + plan.grid - 1) / plan.grid > 64)
         return hipErrorInvalidValue;
     TrainArgs args = a;
     args.grid = plan.grid;
     args.slot_spread = plan.slot_spread;
     args.lds_rows = plan.variant == 3 ? 0 : plan.lds_rows;
-    const int64_t nb = (a.nsteps + pi->m - 1) / pi->m;
-    pi->dots<<<dim3((unsigned)nb), dim3(256), 0, s>>>(args, args.block_dots, nb);
+    const int64_t nb = (a.nsteps + plan.block_m - 1) / plan.block_m;
+    dots<<<dim3((unsigned)nb), dim3(256), 0, s>>>(args, args.block_dots, nb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    PipeKernel fn = plan.variant == 3 ? pi->lds : pipe_stream_kernel(pi->m, pi->ks);
-    if (!fn) return hipErrorInvalidValue;
     void *params[] = {&args};
     return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),
-                                      dim3(256), params, (unsigned)plan.lds_bytes, s);
+                                      dim3(plan.block), params, (unsigned)plan.lds_bytes, s);
 }
 
 }  // namespace som

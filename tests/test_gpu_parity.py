@@ -577,6 +577,32 @@ def test_large_maps_at_small_d_follow_the_oracle(side):
     _train_vs_oracle(side, side, 64, 150, 1)
 
 
+# The streamed pipelined kernel on four sweeper waves (plan block 320):
+# rows of 512 float4, two slices per sweeper (one for the last sweeper when
+# d leaves seven), ragged row counts, 0 to all rows in LDS; and the same
+# shapes forced onto three sweepers.
+@pytest.mark.parametrize("rows,cols,d,n,epochs,grid", [
+    (9, 50, 2048, 40, 1, 0),     # 2 units per workgroup at the planner's grid
+    (11, 12, 2048, 41, 2, 8),    # 16-17 rows per workgroup, partial last block
+    (20, 13, 1500, 61, 2, 8),    # 375 float4 of 512: the last slices partly zero
+    (20, 20, 1100, 17, 1, 8),    # 50 rows per workgroup, d = 1100 (row pitch 2048)
+])
+@pytest.mark.parametrize("lds_rows", ["0", "3", "64"])
+@pytest.mark.parametrize("sweepers", ["4", "3"])
+def test_streamed_pipelined_sweeper_counts_follow_the_oracle(rows, cols, d, n, epochs, grid,
+                                                             lds_rows, sweepers, monkeypatch):
+    if rows * cols / max(grid, 1) > 64:
+        pytest.skip("more than 64 units per workgroup")
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", "4")
+    monkeypatch.setenv("SOM_TRAIN_SWEEPERS", sweepers)
+    monkeypatch.setenv("SOM_TRAIN_LDS_ROWS", lds_rows)
+    if grid:
+        monkeypatch.setenv("SOM_TRAIN_GRID", str(grid))
+    say("streamed sweepers", sweepers, rows, cols, d, n, epochs, "grid", grid, "lds_rows", lds_rows)
+    plan = _train_vs_oracle(rows, cols, d, n, epochs)
+    assert plan["variant"] == 2 and plan["block"] == 64 * (int(sweepers) + 1)
+
+
 # Rows too long for the pipelined kernel's sample registers, on its
 # column-walk sweep (plan variant 4): ragged row counts per workgroup, slices
 # reaching past d (zeros there), sweepers with different slice counts, a
@@ -629,7 +655,7 @@ def test_long_rows_pipelined_hexagonal_and_schedule_edges(monkeypatch):
     (1, 3, 64, 4),     # 20x20, d = 2000
     (2, 3, 256, 2),    # 30x30, d = 5000
     (3, 4, 256, 4),    # 50x50, d = 10000: pipelined, column walk over streamed rows
-    (4, 2, 256, 4),    # 100x100, d = 2048: pipelined, streamed rows
+    (4, 2, 256, 4),    # 100x100, d = 2048: pipelined, streamed rows, four sweepers
 ])
 def test_workload_launch_shapes(ci, variant, grid, block_steps, monkeypatch):
     for var in ("SOM_TRAIN_VARIANT", "SOM_TRAIN_GRID", "SOM_TRAIN_BLOCK_M", "SOM_TRAIN_LDS_ROWS"):
