@@ -191,14 +191,21 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
     constexpr bool DOTS = ADOT || BDOT;
     constexpr int NA = ND + 1;  // f.f, f.x_i, f.xn_j and f.z (last)
     [[maybe_unused]] row_t<LDSW> *rows = rows_as<LDSW>(rows_p);
-    const int lane = threadIdx.x & 63, s = threadIdx.x >> 6;
+    // (the sweeper index as a scalar: derived from the thread index, the
+    // compiler could not prove it uniform, and the buffer resource and its
+    // offsets below would go through per-lane loops)
+    const int lane = threadIdx.x & 63, s = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     // Streamed rows go through a buffer resource over the R rows: a slice
     // past the sweeper's share gets an offset beyond its end, so that its
     // load returns zeros and its store is dropped, with no select or branch
     // (either would make the compiler wait for the row loads in flight).
     // (unused by the LDS variant)
-    const __amdgpu_buffer_rsrc_t rs =
-        __builtin_amdgcn_make_buffer_rsrc(rows_p, (short)0, LDSW ? 0 : R * P4 * 16, 0x00020000);
+    const uint64_t rbase = reinterpret_cast<uintptr_t>(rows_p);
+    f4 *rows_u = reinterpret_cast<f4 *>(
+        ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(rbase >> 32)) << 32) |
+        (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)rbase));
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        rows_u, (short)0, __builtin_amdgcn_readfirstlane(LDSW ? 0 : R * P4 * 16), 0x00020000);
     constexpr int kOutside = 1 << 30;  // bytes, beyond any sweep's rows
     const auto slice_off = [&](int r, int t) {
         return t < nw ? (r * P4 + 64 * (s + NS * t) + lane) * 16 : kOutside;
