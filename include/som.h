@@ -35,6 +35,17 @@
  *     is then lr * exp2(-g * log2(e) / (2 sigma^2)) in fp32 (the hardware
  *     exp2, denormal results flushed to zero), g the squared lattice
  *     distance; QE and TE are accumulated in fp64.
+ *   - Memory cap: SOM_MAX_BYTES (environment, decimal bytes, default 64 GiB,
+ *     read at every call) bounds each buffer a map allocates: the prototypes
+ *     (som_create), the evaluation scratch (candidate lists; three per-sample
+ *     arrays), the sparse and batch work buffers.  A call that would exceed
+ *     it returns SOM_E_OOM before allocating, and the map stays usable.
+ *   - Failure-path switches (environment, for tests of the error paths only):
+ *     SOM_DEBUG_EXCHANGE_TIMEOUT_US bounds each grid-exchange wait of the
+ *     training kernels (default 20 s); SOM_DEBUG_ABSENT_WORKGROUP=1 makes
+ *     som_train launch one workgroup fewer than its exchanges wait for, so
+ *     every wait runs into that bound, every workgroup leaves its loop, and
+ *     the next synchronizing call reports SOM_E_TIMEOUT.
  *   - Device pointer extents are checked against the allocation that holds
  *     the pointer (hipMemGetAddressRange).  Under a pooling allocator (for
  *     example torch's caching allocator) that allocation can be a larger
@@ -58,7 +69,8 @@ typedef enum som_status {
     SOM_E_LAUNCH = 4,      /* the cooperative grid cannot be co-resident    */
     SOM_E_TIMEOUT = 5,     /* a grid barrier did not complete in time       */
     SOM_E_UNSUPPORTED = 6, /* shape outside what the kernels are built for  */
-    SOM_E_BAD_ORDER = 7    /* a caller-supplied sample index was outside [0, n) */
+    SOM_E_BAD_ORDER = 7,   /* a caller-supplied sample index was outside [0, n) */
+    SOM_E_NONFINITE = 8    /* the training data held a NaN or an infinity   */
 } som_status;
 
 /* Lattice of the map.  RECT: unit u = r * cols + c sits at (r, c).  HEX
@@ -144,7 +156,11 @@ som_status som_set_stream(som_map *map, void *stream);
  * and at least 690 otherwise, i.e. 1,048,576 and 176,640 units on 256
  * workgroups), SOM_E_LAUNCH, SOM_E_DEVICE.
  * An order entry outside [0, n) stops the kernel before any update and is
- * reported as SOM_E_BAD_ORDER by the next synchronizing call. */
+ * reported as SOM_E_BAD_ORDER by the next synchronizing call.  Every call
+ * also scans all n * d floats of X once (a read of n * d * 4 bytes): a NaN
+ * or an infinity anywhere in X likewise stops the kernel before any update
+ * and is reported as SOM_E_NONFINITE (the first of the two errors raised
+ * is the one reported). */
 som_status som_train(som_map *map, const float *X, int64_t n, int32_t epochs,
                      const som_schedule *sched);
 
@@ -173,7 +189,8 @@ som_status som_train(som_map *map, const float *X, int64_t n, int32_t epochs,
  * [0, d), indices or values not covering indptr[n] entries),
  * SOM_E_UNSUPPORTED (a row with more than 64 non-zeros, more than 16,384
  * units, or (d + 1) * roundup(rows * cols, 64) * 8 above 2^31 - 1 bytes),
- * SOM_E_OOM (the buffers above beyond the map's memory cap). */
+ * SOM_E_OOM (the buffers above beyond the map's memory cap).  The
+ * indptr[n] values are scanned as som_train scans X (SOM_E_NONFINITE). */
 som_status som_train_csr(som_map *map, const int64_t *indptr, const int32_t *indices,
                          const float *values, int64_t n, int32_t epochs,
                          const som_schedule *sched);

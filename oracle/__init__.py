@@ -18,7 +18,13 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "som_oracle.c")
-_LIB = os.path.join(_HERE, "libsom_oracle.so")
+# SOM_ORACLE_SANITIZE=1 selects an AddressSanitizer + UndefinedBehaviorSanitizer
+# build in a file of its own (the process must have libasan preloaded; see
+# run_sanitized.py beside this file).
+SANITIZE = os.environ.get("SOM_ORACLE_SANITIZE", "") == "1"
+_LIB = os.path.join(_HERE, "libsom_oracle_san.so" if SANITIZE else "libsom_oracle.so")
+SANITIZE_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer",
+                  "-fsanitize=address,undefined", "-fno-sanitize-recover=all"]
 
 RECT, HEX = 0, 1
 LINEAR, EXPONENTIAL = 0, 1
@@ -32,9 +38,11 @@ class Schedule(C.Structure):
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (plain -O2, no fast-math, no FMA contraction)."""
+    """Compile the oracle with gcc (plain -O2, no fast-math, no FMA contraction;
+    with SOM_ORACLE_SANITIZE=1, -O1 under ASan and UBSan instead)."""
     if force or not os.path.exists(_LIB):
-        cmd = ["gcc", "-O2", "-std=gnu11", "-fopenmp", "-ffp-contract=off",
+        opt = SANITIZE_FLAGS if SANITIZE else ["-O2"]
+        cmd = ["gcc", *opt, "-std=gnu11", "-fopenmp", "-ffp-contract=off",
                "-fno-fast-math", "-shared", "-fPIC", "-Wall", "-Wextra",
                "-o", _LIB + ".tmp", _SRC, "-lm"]
         subprocess.run(cmd, check=True)

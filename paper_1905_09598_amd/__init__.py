@@ -39,7 +39,7 @@ LINEAR, EXPONENTIAL = 0, 1
 
 STATUS = {0: "SOM_OK", 1: "SOM_E_ARG", 2: "SOM_E_OOM", 3: "SOM_E_DEVICE",
           4: "SOM_E_LAUNCH", 5: "SOM_E_TIMEOUT", 6: "SOM_E_UNSUPPORTED",
-          7: "SOM_E_BAD_ORDER"}
+          7: "SOM_E_BAD_ORDER", 8: "SOM_E_NONFINITE"}
 
 # Every symbol include/som.h declares.
 EXPORTED = (

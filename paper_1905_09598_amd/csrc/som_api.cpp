@@ -175,6 +175,10 @@ hipError_t ensure(som_map *m, T **p, int64_t *cap, int64_t need) {
 som_status ensure_eval_scratch(som_map *m, int64_t n, int64_t ncand) {
     hipError_t e;
     som_status st;
+    // the candidate lists, and the three per-sample arrays, against the cap
+    if ((uint64_t)ncand * sizeof(int32_t) > max_bytes() ||
+        (uint64_t)n * (2 * sizeof(int32_t) + sizeof(float)) > max_bytes())
+        return SOM_E_OOM;
     if (ncand > m->cand_cap) {
         if ((e = hipStreamSynchronize(m->stream)) != hipSuccess) return from_hip(e);
         m->cand_cap = 0;
@@ -250,6 +254,7 @@ const char *som_status_string(som_status s) {
         case SOM_E_TIMEOUT: return "grid barrier timed out";
         case SOM_E_UNSUPPORTED: return "shape not supported by the built kernels";
         case SOM_E_BAD_ORDER: return "sample order holds an index outside [0, n)";
+        case SOM_E_NONFINITE: return "training data holds a NaN or an infinity";
     }
     return "unknown status";
 }
@@ -397,6 +402,13 @@ static som::TrainArgs train_args(som_map *m, const float *X, int64_t n) {
     a.sweepers = (sw && *sw) ? atoi(sw) : 0;
     if (a.sweepers != 3 && a.sweepers != 4) a.sweepers = 0;
     a.timeout_ticks = 100000000ull * 20;  // 20 s at the 100 MHz reference clock
+    // SOM_DEBUG_EXCHANGE_TIMEOUT_US (failure-path tests): a shorter bound on
+    // each exchange wait, in microseconds.
+    const char *to = getenv("SOM_DEBUG_EXCHANGE_TIMEOUT_US");
+    if (to && *to) {
+        const long long us = atoll(to);
+        if (us > 0 && us < 20000000) a.timeout_ticks = (uint64_t)us * 100;
+    }
     return a;
 }
 
@@ -637,7 +649,13 @@ som_status som_train(som_map *m, const float *X, int64_t n, int32_t epochs,
     }
     a.grid = plan.grid;
     a.slot_spread = plan.slot_spread;
+    // SOM_DEBUG_ABSENT_WORKGROUP=1 (failure-path tests): launch one workgroup
+    // fewer than the exchanges wait for, so that every exchange wait of the
+    // call runs into its time bound and the kernel ends with SOM_E_TIMEOUT.
+    const char *ab = getenv("SOM_DEBUG_ABSENT_WORKGROUP");
+    if (ab && ab[0] == '1' && ab[1] == '\0' && plan.grid > 1) plan.absent = 1;
     e = som::launch_prepare_train(a, m->sched, m->stream);
+    if (e == hipSuccess) e = som::launch_scan_finite(X, n * m->d, m->state, m->stream);
     if (e == hipSuccess) e = som::launch_train(a, plan, m->stream);
     return from_hip(e);
 }
@@ -706,6 +724,7 @@ som_status som_train_csr(som_map *m, const int64_t *indptr, const int32_t *indic
     sp.spv2 = m->spv2;
     sp.sst = m->sst;
     e = som::launch_prepare_train(a, m->sched, m->stream);
+    if (e == hipSuccess && nnz > 0) e = som::launch_scan_finite(values, nnz, m->state, m->stream);
     if (e == hipSuccess) e = som::launch_sparse_steps(a, sp, indptr, indices, values, m->stream);
     if (e == hipSuccess) e = som::launch_sparse_enter(a, sp, m->stream);
     if (e == hipSuccess) e = som::launch_train_sparse(a, sp, m->stream);

@@ -24,7 +24,8 @@ constexpr int64_t kSlotWords = kSlotReplicas * kSlotReplicaStride;
 // Device-side status words of a map (one allocation, zeroed at creation).
 struct DevState {
     int32_t status;     // sticky error code (som_status), cleared by the host
-    int32_t order_bad;  // 1 if the current call's order has an index outside [0, n)
+    int32_t order_bad;  // 1 if the current call's inputs are unusable: an order index
+                        // outside [0, n), or a NaN or infinity in its samples
     int32_t csr_bad;    // 1 if the current call's CSR rows are malformed
     int32_t csr_max_len;  // longest CSR row of the current call
 };
@@ -67,6 +68,8 @@ struct TrainPlan {
                              // sweep): its row bound per workgroup, 0 otherwise
     int32_t slot_spread = 1;
     size_t lds_bytes = 0;
+    int32_t absent = 0;      // workgroups left out of the launch (the failure-path
+                             // tests' host-forced exchange timeout); 0 otherwise
 };
 
 // Squared lattice distance between units u and c of a map with `cols`
@@ -107,6 +110,10 @@ hipError_t launch_init_uniform(float *W, int64_t ld, int32_t N, int32_t d,
 // (raising order_bad and the sticky status) and fill the per-step schedule
 // table from the fp64 decay laws.
 hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, hipStream_t s);
+// After launch_prepare_train: flag (order_bad, status SOM_E_NONFINITE) a NaN
+// or infinity among the `count` floats at x.
+hipError_t launch_scan_finite(const float *x, int64_t count, DevState *state,
+                              hipStream_t s);
 hipError_t launch_row_sqnorm(const float *W, int64_t ld, int32_t N, float *out,
                              hipStream_t s);
 // Copy the n x d rows of X into out, rows of xld floats (xld >= d, a

@@ -545,6 +545,7 @@ hipError_t plan_train(const TrainArgs &a, int num_cus, TrainPlan *plan) {
 }
 
 hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s) {
+    if (plan.absent < 0 || plan.absent >= plan.grid) return hipErrorInvalidValue;
     if (plan.variant >= 2) return launch_train_pipe(a, plan, s);
     const Instance *in = nullptr;
     for (const Instance &c : kInstances)
@@ -559,8 +560,9 @@ hipError_t launch_train(const TrainArgs &a, const TrainPlan &plan, hipStream_t s
     args.lds_rows = plan.variant ? 0 : plan.lds_rows;
     TrainKernel fn = plan.variant ? in->lds : in->stream;
     void *params[] = {&args};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),
-                                      dim3(plan.block), params, (unsigned)plan.lds_bytes, s);
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn),
+                                      dim3(plan.grid - plan.absent), dim3(plan.block), params,
+                                      (unsigned)plan.lds_bytes, s);
 }
 
 }  // namespace som

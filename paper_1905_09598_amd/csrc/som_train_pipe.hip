@@ -295,8 +295,9 @@ hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStrea
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         void *params[] = {&args};
-        return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),
-                                          dim3(256), params, (unsigned)plan.lds_bytes, s);
+        return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn),
+                                          dim3(plan.grid - plan.absent), dim3(256), params,
+                                          (unsigned)plan.lds_bytes, s);
     }
     const int ns = plan.block / 64 - 1;
     if (ns != 3 && ns != 4) return hipErrorInvalidValue;
@@ -319,8 +320,9 @@ hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStrea
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     void *params[] = {&args};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn), dim3(plan.grid),
-                                      dim3(plan.block), params, (unsigned)plan.lds_bytes, s);
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(fn),
+                                      dim3(plan.grid - plan.absent), dim3(plan.block), params,
+                                      (unsigned)plan.lds_bytes, s);
 }
 
 }  // namespace som

@@ -1,6 +1,6 @@
 // Small helper kernels: prototype initialisation, per-call preparation of
-// the training kernel (exchange slots, order check, schedule table), row
-// squared norms.
+// the training kernel (exchange slots, order check, schedule table), the
+// non-finite scan of training data, row squared norms.
 #include "som_internal.h"
 
 namespace som {
@@ -82,6 +82,40 @@ __global__ void prepare_train_kernel(const int32_t *order, int64_t nsteps, int64
     sched[s] = make_float2((float)lr, (float)c2);
 }
 
+// Raise the call's input flag (which stops the training kernels before any
+// update) and the sticky status, SOM_E_NONFINITE unless an error is pending,
+// when any of the `count` floats at x is a NaN or an infinity (all exponent
+// bits set).  One read of x: 16-byte loads, four in flight per thread.
+__global__ void scan_finite_kernel(const float *x, int64_t count, DevState *state) {
+    constexpr unsigned kExp = 0x7f800000u;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    const unsigned *xu = reinterpret_cast<const unsigned *>(x);
+    bool bad = false;
+    int64_t tail = 0;  // first element the vector loop leaves to the scalar one
+    if (reinterpret_cast<uintptr_t>(x) % 16 == 0) {
+        const uint4 *x4 = reinterpret_cast<const uint4 *>(x);
+        const int64_t n4 = count / 4;
+        const auto nonfinite4 = [&](const uint4 v) {
+            return ((v.x & kExp) == kExp) | ((v.y & kExp) == kExp) | ((v.z & kExp) == kExp) |
+                   ((v.w & kExp) == kExp);
+        };
+        int64_t i = t;
+        for (; i + 3 * stride < n4; i += 4 * stride) {
+            const uint4 a = x4[i], b = x4[i + stride], c = x4[i + 2 * stride],
+                        d = x4[i + 3 * stride];
+            bad |= nonfinite4(a) | nonfinite4(b) | nonfinite4(c) | nonfinite4(d);
+        }
+        for (; i < n4; i += stride) bad |= nonfinite4(x4[i]);
+        tail = n4 * 4;
+    }
+    for (int64_t i = tail + t; i < count; i += stride) bad |= (xu[i] & kExp) == kExp;
+    if (__ballot(bad) != 0 && (threadIdx.x & 63) == 0) {
+        atomicOr(&state->order_bad, 1);
+        atomicCAS(&state->status, 0, 8);  // SOM_E_NONFINITE unless an error is pending
+    }
+}
+
 // out[u] = sum_j W[u][j]^2, one wave per row (fp32, fixed order).
 __global__ void row_sqnorm_kernel(const float *W, int64_t ld, int32_t N, float *out) {
     const int lane = threadIdx.x & 63;
@@ -128,6 +162,16 @@ hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, hipStream_t s
     prepare_train_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(
         a.order, a.nsteps, a.n, a.step0, a.total_steps, a.lr0, a.lr1, a.lr_decay, a.sigma0,
         a.sigma1, a.sigma_decay, sched, a.state);
+    return hipGetLastError();
+}
+
+hipError_t launch_scan_finite(const float *x, int64_t count, DevState *state,
+                              hipStream_t s) {
+    if (count <= 0) return hipSuccess;
+    int64_t blocks = (count / 4 + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    if (blocks < 1) blocks = 1;
+    scan_finite_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(x, count, state);
     return hipGetLastError();
 }
 

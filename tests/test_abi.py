@@ -28,11 +28,32 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, name), name
 
 
+def header_status_codes():
+    body = re.search(r"typedef enum som_status \{(.*?)\} som_status;", open(HEADER).read(),
+                     flags=re.S).group(1)
+    return {int(v): k for k, v in re.findall(r"(SOM_\w+)\s*=\s*(\d+)", body)}
+
+
 def test_status_strings():
+    codes = header_status_codes()
+    assert codes == som.STATUS                     # the binding's names are the header's
+    assert codes[8] == "SOM_E_NONFINITE" and codes[5] == "SOM_E_TIMEOUT"
     assert som.som_status_string(0) == "ok"
-    for code in range(1, 8):
-        assert som.som_status_string(code) not in ("", "unknown status")
+    texts = {som.som_status_string(code) for code in codes if code}
+    assert len(texts) == len(codes) - 1 and "unknown status" not in texts
     assert som.som_status_string(99) == "unknown status"
+
+
+def test_memory_cap_refuses_a_map_before_device_work(monkeypatch):
+    # a 10 x 10 map of d = 64 needs 100 rows of at least 64 floats
+    monkeypatch.setenv("SOM_MAX_BYTES", str(100 * 64 * 4 - 1))
+    with pytest.raises(som.SomError) as e:
+        som.som_create(10, 10, 64, 0)
+    assert e.value.name == "SOM_E_OOM"
+    monkeypatch.setenv("SOM_MAX_BYTES", "1")
+    with pytest.raises(som.SomError) as e:
+        som.som_create(1, 1, 1, 0)
+    assert e.value.name == "SOM_E_OOM"
 
 
 @pytest.mark.parametrize("rows,cols,d", [(0, 3, 4), (3, 0, 4), (3, 3, 0), (-1, 2, 2),
