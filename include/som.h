@@ -219,7 +219,12 @@ som_status som_train_batch(som_map *map, const float *X, int64_t n, int32_t epoc
 /* Batched BMU assignment (Sec. 8A): for each of the n rows of the device
  * matrix X, out_idx[i] = BMU index (lowest index among equal minima).
  * Candidates are ranked with fp32 matrix-core products
- * ||w||^2 - 2 x.w and the best few re-ranked by direct fp32 distances.
+ * ||w||^2 - 2 x.w (the product split over ranges of d, and the ranges
+ * summed in order, when there are too few samples to fill the chip
+ * otherwise); the four best by that score are re-ranked by direct fp32
+ * distances.  Scratch (candidate lists of 32 bytes per sample and unit
+ * group, or 512 bytes per sample, range and 128 units of partial products
+ * when d is split) is kept by the map.
  * out_idx is a device int32 array of n entries.  Stream-ordered. */
 som_status som_bmu(som_map *map, const float *X, int64_t n, int32_t *out_idx);
 
@@ -233,13 +238,20 @@ som_status som_bmu2(som_map *map, const float *X, int64_t n, int32_t *out_idx,
  * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
  * the same kernels and the same outputs, but no hipMalloc, hipFree or
  * allocating library routine is called.  The call's scratch (the
- * prototypes' squared norms, the candidate lists, and the BMUs when
- * out_idx is NULL) lives in one fixed 8 MiB array per device, held from
- * the library's load until the process ends; it needs
- *     roundup256(4 N) + roundup256(16 n G) + (out_idx ? 0 : roundup256(4 n))
- * bytes (N units, G the unit groups of the candidate search: 1 when
- * n >= 32705, at most roundup(N, 128) / 128 below), and a call whose
- * inputs need more returns SOM_E_UNSUPPORTED without launching anything.
+ * prototypes' squared norms, the BMUs when out_idx is NULL, the candidate
+ * lists, and the partial products when the search splits d) lives in one
+ * fixed 8 MiB array per device, held from the library's load until the
+ * process ends.  The search takes the fastest shape whose scratch fits:
+ *     roundup256(4 N) + (out_idx ? 0 : roundup256(4 n))
+ *       + (split ? roundup256(512 S n T_u) : roundup256(32 n G))
+ * bytes (N units; unsplit, G the unit groups whose candidate lists are kept
+ * apart; split, S the ranges of d and T_u = ceil(N / 128) the unit tiles);
+ * with G = 1 and no split the need is smallest, and a call whose inputs
+ * need more than the array even then
+ * returns SOM_E_UNSUPPORTED without launching anything.  The outputs equal
+ * som_bmu2's whenever the same shape fits (the shape is chosen from the
+ * sizes alone), and otherwise whenever a sample's best two units are not
+ * tied with its fifth by score within rounding.
  * Every call on a device shares that device's array and overwrites what
  * it needs before reading it, so calls that overlap on one device (on
  * different streams, or from different host threads) race; order them.

@@ -59,6 +59,8 @@ struct som_map {
     float *wnorm = nullptr;
     int32_t *cand = nullptr, *idx1 = nullptr, *idx2 = nullptr;
     int64_t cand_cap = 0;
+    float *part = nullptr;
+    int64_t part_cap = 0;
     float *d1 = nullptr;
     double *sums = nullptr;
     int64_t eval_cap = 0;
@@ -168,15 +170,17 @@ hipError_t ensure(som_map *m, T **p, int64_t *cap, int64_t need) {
     return e;
 }
 
-// Evaluation scratch for n samples and ncand candidates.  A capacity is
-// zeroed before its buffers are replaced and set again only once every one
-// of them is allocated, so a failed allocation leaves no stale capacity
-// behind a null or freed buffer.
-som_status ensure_eval_scratch(som_map *m, int64_t n, int64_t ncand) {
+// Evaluation scratch for n samples, ncand candidate-list entries (int32)
+// and npart partial products.  A capacity is zeroed before its buffers are
+// replaced and set again only once every one of them is allocated, so a
+// failed allocation leaves no stale capacity behind a null or freed buffer.
+som_status ensure_eval_scratch(som_map *m, int64_t n, int64_t ncand, int64_t npart = 0) {
     hipError_t e;
     som_status st;
-    // the candidate lists, and the three per-sample arrays, against the cap
+    // the candidate lists, the partial products and the three per-sample
+    // arrays, each against the cap
     if ((uint64_t)ncand * sizeof(int32_t) > max_bytes() ||
+        (uint64_t)npart * sizeof(float) > max_bytes() ||
         (uint64_t)n * (2 * sizeof(int32_t) + sizeof(float)) > max_bytes())
         return SOM_E_OOM;
     if (ncand > m->cand_cap) {
@@ -184,6 +188,12 @@ som_status ensure_eval_scratch(som_map *m, int64_t n, int64_t ncand) {
         m->cand_cap = 0;
         if ((st = grow(&m->cand, ncand)) != SOM_OK) return st;
         m->cand_cap = ncand;
+    }
+    if (npart > m->part_cap) {
+        if ((e = hipStreamSynchronize(m->stream)) != hipSuccess) return from_hip(e);
+        m->part_cap = 0;
+        if ((st = grow(&m->part, npart)) != SOM_OK) return st;
+        m->part_cap = npart;
     }
     if (n <= m->eval_cap) return SOM_OK;
     if ((e = hipStreamSynchronize(m->stream)) != hipSuccess) return from_hip(e);
@@ -220,11 +230,12 @@ som_status run_eval(som_map *m, const float *X, int64_t n, int32_t *idx1,
     a.topology = m->topology;
     a.X = X;
     a.n = n;
-    som::plan_bmu_candidates(&a);
-    som_status st = ensure_eval_scratch(m, n, n * a.ugroups * som::kCand);
+    if (!som::plan_bmu_candidates(&a, m->num_cus, max_bytes())) return SOM_E_OOM;
+    som_status st = ensure_eval_scratch(m, n, som::bmu_cand_ints(a), som::bmu_part_floats(a));
     if (st != SOM_OK) return st;
     a.wnorm = m->wnorm;
     a.cand = m->cand;
+    a.part = m->part;
     a.idx1 = idx1;
     a.idx2 = idx2;
     a.d1 = d1;
@@ -331,6 +342,7 @@ som_status som_destroy(som_map *m) {
     (void)hipFree(m->sst);
     (void)hipFree(m->wnorm);
     (void)hipFree(m->cand);
+    (void)hipFree(m->part);
     (void)hipFree(m->idx1);
     (void)hipFree(m->idx2);
     (void)hipFree(m->d1);
@@ -813,21 +825,30 @@ som_status som_bmu2_noalloc(som_map *m, const float *X, int64_t n, int32_t *out_
     a.topology = m->topology;
     a.X = X;
     a.n = n;
-    som::plan_bmu_candidates(&a);
-    // scratch layout: prototype norms | candidates | BMUs when out_idx is NULL
+    // scratch layout: prototype norms | BMUs when out_idx is NULL | candidate
+    // lists | partial products, each rounded up to 256 bytes; the search
+    // takes the best shape that fits what the first two leave
     const auto round256 = [](uint64_t b) { return (b + 255) / 256 * 256; };
     const uint64_t norm_bytes = round256((uint64_t)m->N * 4);
-    const uint64_t cand_bytes = round256((uint64_t)n * (uint64_t)a.ugroups * som::kCand * 4);
     const uint64_t idx_bytes = out_idx ? 0 : round256((uint64_t)n * 4);
-    if (norm_bytes + cand_bytes + idx_bytes > som::kNoAllocScratchBytes) return SOM_E_UNSUPPORTED;
+    if (norm_bytes + idx_bytes + 512 > som::kNoAllocScratchBytes) return SOM_E_UNSUPPORTED;
+    if (!som::plan_bmu_candidates(&a, m->num_cus,
+                                  som::kNoAllocScratchBytes - norm_bytes - idx_bytes - 512))
+        return SOM_E_UNSUPPORTED;
+    const uint64_t cand_bytes = round256((uint64_t)som::bmu_cand_ints(a) * 4);
+    const uint64_t part_bytes = round256((uint64_t)som::bmu_part_floats(a) * 4);
+    if (norm_bytes + idx_bytes + cand_bytes + part_bytes > som::kNoAllocScratchBytes)
+        return SOM_E_UNSUPPORTED;
     void *base = nullptr;
     e = som::noalloc_scratch(&base);
     if (e != hipSuccess) return from_hip(e);
     unsigned char *p = static_cast<unsigned char *>(base);
     float *wnorm = reinterpret_cast<float *>(p);
     a.wnorm = wnorm;
-    a.cand = reinterpret_cast<int32_t *>(p + norm_bytes);
-    a.idx1 = out_idx ? out_idx : reinterpret_cast<int32_t *>(p + norm_bytes + cand_bytes);
+    a.cand = reinterpret_cast<int32_t *>(p + norm_bytes + idx_bytes);
+    a.part = part_bytes ? reinterpret_cast<float *>(p + norm_bytes + idx_bytes + cand_bytes)
+                        : nullptr;
+    a.idx1 = out_idx ? out_idx : reinterpret_cast<int32_t *>(p + norm_bytes);
     a.idx2 = out_idx2;
     a.d1 = out_d1;
     a.x_vec4 = (m->d % 4 == 0) && (reinterpret_cast<uintptr_t>(X) % 16 == 0);

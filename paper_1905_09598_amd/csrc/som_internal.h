@@ -114,6 +114,7 @@ hipError_t launch_prepare_train(const TrainArgs &a, float2 *sched, hipStream_t s
 // or infinity among the `count` floats at x.
 hipError_t launch_scan_finite(const float *x, int64_t count, DevState *state,
                               hipStream_t s);
+// out[u] = |W[u]|^2 for the N rows of W.
 hipError_t launch_row_sqnorm(const float *W, int64_t ld, int32_t N, float *out,
                              hipStream_t s);
 // Copy the n x d rows of X into out, rows of xld floats (xld >= d, a
@@ -128,9 +129,13 @@ struct EvalArgs {
     const float *X;
     int64_t n;
     const float *wnorm;     // N squared prototype norms
-    int32_t *cand;          // n x ugroups x kCand candidate units (scratch)
-    int32_t ugroups;        // unit groups searched by separate workgroups
+    int32_t *cand;          // n x ugroups x kCand (score bits, unit) pairs (scratch)
+    int32_t ugroups;        // unit groups whose lists are kept apart
     int32_t group_units;    // units per group (a multiple of the unit tile)
+    int32_t splits;         // ranges of d computed by separate workgroups (1: fused)
+    int32_t split_len;      // columns per range (a multiple of the slice width)
+    int32_t tiles_s, tiles_u;  // sample and unit tiles
+    float *part;            // splits > 1: splits x n x (tiles_u x 128) partial products
     int32_t *idx1;          // n (required)
     int32_t *idx2;          // n (nullable)
     float *d1;              // n (nullable)
@@ -138,9 +143,16 @@ struct EvalArgs {
 };
 constexpr int kCand = 4;
 
-// Unit groups for n samples over N units: enough workgroups to fill the
-// chip when n is small (sets a->ugroups and a->group_units).
-void plan_bmu_candidates(EvalArgs *a);
+// The candidate search's shape for n samples over N units on `num_cus`
+// compute units (sets ugroups, group_units, splits, split_len, tiles_s,
+// tiles_u): the fewest rounds of workgroups, among the shapes whose
+// candidate lists and partial products fit in max_scratch_bytes.  False
+// when none does.
+bool plan_bmu_candidates(EvalArgs *a, int num_cus, uint64_t max_scratch_bytes);
+// Scratch of a planned search: int32 entries of the candidate lists and
+// floats of the partial products (0 for the fused form).
+int64_t bmu_cand_ints(const EvalArgs &a);
+int64_t bmu_part_floats(const EvalArgs &a);
 hipError_t launch_bmu_candidates(const EvalArgs &a, hipStream_t s);
 // Fixed per-device scratch of som_bmu2_noalloc (som_eval.hip): its device
 // address on the current device, looked up once per device.

@@ -147,7 +147,10 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
     // waves instead of three, on every SIMD, the controller beside the
     // first sweeper.  Cost as above with the four-sweeper slice count and
     // the first sweeper's rows 12 % slower (the controller's issue slots
-    // on its SIMD).
+    // on its SIMD).  Only where rows are streamed (unless four sweepers are
+    // asked for): with every row in LDS the LDS-resident kernel, whose
+    // exchanges keep four polls in flight, measured faster (20 x 20 map,
+    // d = 2000, 64 workgroups: 1.29 against 1.74 us per step).
     for (const Wide &wi : kWide) {
         const int ks4 = (nsl + 3) / 4;
         if (wi.ks != ks4 || a.variant == 1 || a.sweepers == 3 ||
@@ -163,7 +166,7 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                 rl = (int)(fit < rmax ? fit : rmax);
                 if (a.lds_rows >= 0) rl = a.lds_rows < rl ? a.lds_rows : rl;
             }
-            if (rmax <= 64 && base <= (size_t)max_lds) {
+            if (rmax <= 64 && base <= (size_t)max_lds && (rl < rmax || a.sweepers == 4)) {
                 const double row_us = 1.12 * (ks4 * (0.027 * wi.m + 0.0395) + 0.012 * wi.m + 0.0665);
                 const double blk_us = rmax * row_us + (rmax - rl) * 0.05 + 0.5 + 0.15 * wi.m;
                 const double mem_us = (rmax - rl) * P4 * 32.0 / (8e6 / gg);

@@ -116,17 +116,36 @@ __global__ void scan_finite_kernel(const float *x, int64_t count, DevState *stat
     }
 }
 
-// out[u] = sum_j W[u][j]^2, one wave per row (fp32, fixed order).
-__global__ void row_sqnorm_kernel(const float *W, int64_t ld, int32_t N, float *out) {
-    const int lane = threadIdx.x & 63;
-    const int64_t row = blockIdx.x * (int64_t)(blockDim.x / 64) + (threadIdx.x >> 6);
-    if (row >= N) return;
-    const float *w = W + row * ld;
+// out[u] = sum_j W[u][j]^2 (fp32, fixed order): `tpr` threads per row (64,
+// 128 or 256; 256 / tpr rows per workgroup), 16-byte loads, four in flight.
+__global__ __launch_bounds__(256) void row_sqnorm_kernel(const float *W, int64_t ld, int32_t N,
+                                                         float *out, int tpr) {
+    __shared__ float part[4];
+    const int rsub = threadIdx.x / tpr, t = threadIdx.x - rsub * tpr;
+    const int64_t row = (int64_t)blockIdx.x * (256 / tpr) + rsub;
     float acc = 0.f;
-    for (int64_t j = lane; j < ld; j += 64) acc = fmaf(w[j], w[j], acc);
+    if (row < N) {
+        const float4 *w = reinterpret_cast<const float4 *>(W + row * ld);
+        const int64_t n4 = ld / 4;
+#pragma unroll 4
+        for (int64_t j = t; j < n4; j += tpr) {
+            const float4 v = w[j];
+            acc = fmaf(v.x, v.x, acc);
+            acc = fmaf(v.y, v.y, acc);
+            acc = fmaf(v.z, v.z, acc);
+            acc = fmaf(v.w, v.w, acc);
+        }
+    }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
-    if (lane == 0) out[row] = acc;
+    if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (t == 0 && row < N) {
+        const int w0 = threadIdx.x >> 6, nw = tpr / 64;
+        float s = part[w0];
+        for (int k = 1; k < nw; ++k) s += part[w0 + k];
+        out[row] = s;
+    }
 }
 
 __global__ void pad_rows_kernel(const float *X, int64_t n, int32_t d, float *out, int64_t xld) {
@@ -177,9 +196,10 @@ hipError_t launch_scan_finite(const float *x, int64_t count, DevState *state,
 
 hipError_t launch_row_sqnorm(const float *W, int64_t ld, int32_t N, float *out,
                              hipStream_t s) {
-    const int waves = 4;
-    const int64_t blocks = (N + waves - 1) / waves;
-    row_sqnorm_kernel<<<dim3((unsigned)blocks), dim3(64 * waves), 0, s>>>(W, ld, N, out);
+    const int64_t n4 = ld / 4;
+    const int tpr = n4 > 512 ? 256 : n4 > 128 ? 128 : 64;
+    const int64_t blocks = ((int64_t)N + 256 / tpr - 1) / (256 / tpr);
+    row_sqnorm_kernel<<<dim3((unsigned)blocks), dim3(256), 0, s>>>(W, ld, N, out, tpr);
     return hipGetLastError();
 }
 

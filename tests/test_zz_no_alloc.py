@@ -61,7 +61,7 @@ def test_noalloc_rejects_inputs_beyond_its_scratch():
     torch = torch_cuda()
     L = som.lib()
     m = som.Map(16, 16, 64, seed=0)
-    # 16 x 256 units, n = 600,000 > 8 MiB of candidates (16 bytes each)
+    # 16 x 256 units, n = 600,000 > 8 MiB of candidate lists (32 bytes a sample)
     n = 600000
     X = torch.zeros((n, 64), dtype=torch.float32, device="cuda")
     i1 = torch.empty(n, dtype=torch.int32, device="cuda")
