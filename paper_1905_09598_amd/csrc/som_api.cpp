@@ -307,7 +307,9 @@ som_status som_create(int32_t rows, int32_t cols, int32_t d, uint64_t seed,
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&m->slots),
                       (size_t)som::kSlotWords * sizeof(unsigned long long));
-    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->wnorm), (size_t)N * sizeof(float));
+    // prototype norms, roundup(N, 4) floats: the re-rank reads them as float4
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&m->wnorm), (size_t)((N + 3) & ~3) * sizeof(float));
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&m->sums), 2 * sizeof(double));
     if (e == hipSuccess) e = hipEventCreateWithFlags(&m->order_done, hipEventDisableTiming);
     if (e == hipSuccess) e = som::launch_init_uniform(m->W, ld, m->N, d, seed, nullptr);

@@ -336,10 +336,16 @@ __global__ __launch_bounds__(64 * kRerankWaves) void bmu_rerank_kernel(EvalArgs 
         const int nq = (a.N + 3) / 4;
         const f4 *row = reinterpret_cast<const f4 *>(a.part + i * np);
         const int64_t zstride = (int64_t)a.n * np / 4;
+        // (the norms are read as float4: the array holds roundup(N, 4) floats)
+        const f4 *wn4 = reinterpret_cast<const f4 *>(a.wnorm);
         for (int q0 = 0; q0 < nq; q0 += 64 * 4) {
-            f4 dot[4];
+            f4 dot[4], wn[4];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) dot[k] = f4{0.f, 0.f, 0.f, 0.f};
+            for (int k = 0; k < 4; ++k) {
+                const int q = q0 + lane + 64 * k;
+                dot[k] = f4{0.f, 0.f, 0.f, 0.f};
+                wn[k] = q < nq ? wn4[q] : f4{0.f, 0.f, 0.f, 0.f};
+            }
             for (int z = 0; z < a.splits; ++z) {
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
@@ -356,7 +362,7 @@ __global__ __launch_bounds__(64 * kRerankWaves) void bmu_rerank_kernel(EvalArgs 
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int u = 4 * q + e;
-                    if (q < nq && u < a.N) insert_top(ls, lu, a.wnorm[u] - 2.f * dot[k][e], u);
+                    if (q < nq && u < a.N) insert_top(ls, lu, wn[k][e] - 2.f * dot[k][e], u);
                 }
             }
         }

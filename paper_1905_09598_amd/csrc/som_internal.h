@@ -128,7 +128,7 @@ struct EvalArgs {
     int32_t N, d, rows, cols, topology;
     const float *X;
     int64_t n;
-    const float *wnorm;     // N squared prototype norms
+    const float *wnorm;     // N squared prototype norms (roundup(N, 4) floats allocated)
     int32_t *cand;          // n x ugroups x kCand (score bits, unit) pairs (scratch)
     int32_t ugroups;        // unit groups whose lists are kept apart
     int32_t group_units;    // units per group (a multiple of the unit tile)
