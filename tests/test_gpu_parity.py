@@ -645,24 +645,3 @@ def test_long_rows_pipelined_hexagonal_and_schedule_edges(monkeypatch):
     assert np.array_equal(trace.cpu().numpy(), tr)
     assert np.array_equal(m.weights.cpu().numpy().astype(np.float64), Wo)
     m.close()
-
-
-# The launch shapes the planner picks for the five workloads, as measured
-# fastest on MI355X (grid sweeps and block lengths at each workload): a
-# change of cost model that moves one of them shows up here.
-@pytest.mark.parametrize("ci,variant,grid,block_steps", [
-    (0, 3, 8, 4),      # 10x10, d = 500: pipelined, LDS rows
-    (1, 3, 64, 4),     # 20x20, d = 2000
-    (2, 3, 256, 2),    # 30x30, d = 5000
-    (3, 4, 256, 4),    # 50x50, d = 10000: pipelined, column walk over streamed rows
-    (4, 2, 256, 4),    # 100x100, d = 2048: pipelined, streamed rows, four sweepers
-])
-def test_workload_launch_shapes(ci, variant, grid, block_steps, monkeypatch):
-    for var in ("SOM_TRAIN_VARIANT", "SOM_TRAIN_GRID", "SOM_TRAIN_BLOCK_M", "SOM_TRAIN_LDS_ROWS"):
-        monkeypatch.delenv(var, raising=False)
-    cfg = workloads.WORKLOADS[ci]
-    m = som.Map(cfg.rows, cfg.cols, cfg.d, seed=0)
-    plan = m.plan()
-    say("workload", cfg.name, "plan", plan)
-    m.close()
-    assert (plan["variant"], plan["grid"], plan["block_steps"]) == (variant, grid, block_steps)
