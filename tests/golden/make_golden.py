@@ -32,6 +32,8 @@ def main():
     ap.add_argument("config", type=int)
     ap.add_argument("--threads", type=int, default=oracle.default_threads())
     ap.add_argument("--topology", choices=("rect", "hex"), default="rect")
+    ap.add_argument("--out-dir", default=os.path.join(ROOT, "tests", "golden"),
+                    help="directory of the record (default: tests/golden)")
     ap.add_argument("--epoch-qe", action="store_true",
                     help="also record the quantization error after every epoch")
     args = ap.parse_args()
@@ -88,7 +90,8 @@ def main():
         "host": platform.processor() or platform.machine(),
     }
     suffix = "_hex" if args.topology == "hex" else ""
-    path = os.path.join(ROOT, "tests", "golden", f"e2e_{cfg.name}{suffix}.json")
+    os.makedirs(args.out_dir, exist_ok=True)
+    path = os.path.join(args.out_dir, f"e2e_{cfg.name}{suffix}.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1)
         f.write("\n")

@@ -18,7 +18,8 @@ the near ties, and those runs end with the stored TE.)
     python tests/golden/make_te_spread.py CONFIG_INDEX --runs K [--first k0]
         [--threads T] [--topology hex]
 
-appends runs k0 .. k0+K-1 to tests/golden/te_spread_<config name>.json
+appends runs k0 .. k0+K-1 to te_spread_<config name>.json in --out-dir
+(default tests/golden)
 (..._hex.json for the hexagonal lattice), one record per finished training,
 so an interrupted series keeps what it finished.
 """
@@ -64,6 +65,8 @@ def main():
     ap.add_argument("--first", type=int, default=1)
     ap.add_argument("--threads", type=int, default=oracle.default_threads())
     ap.add_argument("--topology", choices=("rect", "hex"), default="rect")
+    ap.add_argument("--out-dir", default=os.path.join(ROOT, "tests", "golden"),
+                    help="directory of the record (default: tests/golden)")
     args = ap.parse_args()
     cfg = workloads.WORKLOADS[args.config]
     topo = oracle.HEX if args.topology == "hex" else oracle.RECT
@@ -72,7 +75,8 @@ def main():
     s = oracle.schedule(cfg.lr0, cfg.lr1, cfg.sigma0, cfg.sigma1,
                         oracle.LINEAR, oracle.EXPONENTIAL)
     suffix = "_hex" if args.topology == "hex" else ""
-    path = os.path.join(ROOT, "tests", "golden", f"te_spread_{cfg.name}{suffix}.json")
+    os.makedirs(args.out_dir, exist_ok=True)
+    path = os.path.join(args.out_dir, f"te_spread_{cfg.name}{suffix}.json")
     header = {
         "written_by": "tests/golden/make_te_spread.py (fp64 oracle only)",
         "config": cfg.name, "n": cfg.n, "topology": args.topology,
