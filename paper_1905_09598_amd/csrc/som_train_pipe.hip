@@ -62,13 +62,13 @@ struct ColsInstance {
 };
 const ColsInstance kCols[] = {{4, 10}};
 
-// Streamed instances on four sweepers (block length, slices per sweeper):
-// every SIMD sweeps, the controller shares the first one
-// (som_train_pipe_stream.hip).
+// Streamed instances on four sweepers (block length, slices per sweeper,
+// rows held in the sweepers' registers): every SIMD sweeps, the controller
+// shares the first one (som_train_pipe_stream.hip).
 struct Wide {
-    int m, ks;
+    int m, ks, rr;
 };
-const Wide kWide[] = {{4, 2}};
+const Wide kWide[] = {{4, 2, kWideRegRows}};
 
 // Measured exchange latency of the pipelined kernel (multi-poll, per-XCD
 // replicated slots) by grid size, in microseconds.
@@ -150,7 +150,10 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
     // on its SIMD).  Only where rows are streamed (unless four sweepers are
     // asked for): with every row in LDS the LDS-resident kernel, whose
     // exchanges keep four polls in flight, measured faster (20 x 20 map,
-    // d = 2000, 64 workgroups: 1.29 against 1.74 us per step).
+    // d = 2000, 64 workgroups: 1.29 against 1.74 us per step).  The first
+    // wi.rr rows past the LDS ones stay in the sweepers' registers for the
+    // whole launch (100 x 100 map, d = 2048: 5.04 -> 4.81 us per step with
+    // two), and only the rest stream.
     for (const Wide &wi : kWide) {
         const int ks4 = (nsl + 3) / 4;
         if (wi.ks != ks4 || a.variant == 1 || a.sweepers == 3 ||
@@ -166,10 +169,12 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                 rl = (int)(fit < rmax ? fit : rmax);
                 if (a.lds_rows >= 0) rl = a.lds_rows < rl ? a.lds_rows : rl;
             }
+            // rows past the LDS ones: up to wi.rr in registers, the rest streamed
+            const int rs = rmax - rl - wi.rr > 0 ? rmax - rl - wi.rr : 0;
             if (rmax <= 64 && base <= (size_t)max_lds && (rl < rmax || a.sweepers == 4)) {
                 const double row_us = 1.12 * (ks4 * (0.027 * wi.m + 0.0395) + 0.012 * wi.m + 0.0665);
-                const double blk_us = rmax * row_us + (rmax - rl) * 0.05 + 0.5 + 0.15 * wi.m;
-                const double mem_us = (rmax - rl) * P4 * 32.0 / (8e6 / gg);
+                const double blk_us = rmax * row_us + rs * 0.05 + 0.5 + 0.15 * wi.m;
+                const double mem_us = rs * P4 * 32.0 / (8e6 / gg);
                 const double sweep = (blk_us > mem_us ? blk_us : mem_us) / wi.m;
                 const double ctl = pipe_exchange_us(gg) + 0.03 * wi.m + 0.36 / wi.m;
                 const double t = sweep > ctl ? sweep : ctl;

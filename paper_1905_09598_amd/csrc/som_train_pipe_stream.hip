@@ -19,7 +19,7 @@ PipeKernel pipe_stream_kernel(int m, int ks, int ns) {
         {8, 1, 3, train_pipe_kernel<8, 1, false>}, {4, 1, 3, train_pipe_kernel<4, 1, false>},
         {4, 2, 3, train_pipe_kernel<4, 2, false>}, {4, 3, 3, train_pipe_kernel<4, 3, false>},
         {2, 3, 3, train_pipe_kernel<2, 3, false>}, {2, 4, 3, train_pipe_kernel<2, 4, false>},
-        {4, 2, 4, train_pipe_kernel<4, 2, false, 0, 4>},
+        {4, 2, 4, train_pipe_kernel<4, 2, false, 0, 4, kWideRegRows>},
     };
     for (const Entry &e : kStream)
         if (e.m == m && e.ks == ks && e.ns == ns) return e.fn;
