@@ -56,10 +56,6 @@ using namespace dev;
 // sweeps) puts every SIMD to sweeping and the controller beside sweeper 0.
 constexpr int kSweepers = 3;
 constexpr int kPipeHeader = 64;
-// Rows per workgroup the four-sweeper streamed kernel keeps in its
-// sweepers' registers (after the LDS rows, before the streamed ones): the
-// most that leave its 256 registers per lane without spills.
-constexpr int kWideRegRows = 2;
 
 template <int M>
 constexpr int dots_stride() { return M * (M + 1) + M * M; }  // AA (T), AB (M*M), BB (T)
@@ -314,97 +310,21 @@ __device__ inline void pipe_sweep(f4 *rows_p, int R, int P4, int nw, const f4 (&
     }
 }
 
-// Rows held in the sweepers' registers for the whole launch: wreg[k][t] is
-// this lane's 16 bytes of slice s + NS t of row k (zero past the sweeper's
-// slices).  The same arithmetic as pipe_sweep, on Rr <= RR rows.
-template <int M, int KS, int RR, bool MAT, bool ADOT, bool BDOT, int NS>
-__device__ inline void reg_sweep(f4 (&wreg)[RR > 0 ? RR : 1][KS], int Rr, const f4 (&xp)[M][KS],
-                                 const f4 (&xc)[M][KS], const f4 (&xn)[M][KS],
-                                 const float *coef_prev, float *dots) {
-    constexpr int ND = 2 * M;
-    constexpr bool DOTS = ADOT || BDOT;
-    constexpr int NA = ND + 1;
-    const int lane = threadIdx.x & 63, s = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-#pragma unroll
-    for (int k = 0; k < RR; ++k) {
-        if (k >= Rr) break;  // (RR = 0: no register rows)
-        float c[M + 1];
-        if (MAT) {
-#pragma unroll
-            for (int i = 0; i <= M; ++i) c[i] = coef_prev[k * (M + 1) + i];
-        }
-        float acc[NA];
-#pragma unroll
-        for (int t = 0; t < NA; ++t) acc[t] = 0.f;
-#pragma unroll
-        for (int t = 0; t < KS; ++t) {
-            f4 w = wreg[k][t];
-            if (MAT) {
-                w = w * c[0];
-#pragma unroll
-                for (int i = 0; i < M; ++i) {
-                    const float g = c[1 + i];
-                    w.x = fmaf(g, xp[i][t].x, w.x);
-                    w.y = fmaf(g, xp[i][t].y, w.y);
-                    w.z = fmaf(g, xp[i][t].z, w.z);
-                    w.w = fmaf(g, xp[i][t].w, w.w);
-                }
-                wreg[k][t] = w;
-            }
-            if (DOTS) {
-                const f4 z = xc[0][t];
-                const f4 f = w - z;
-                acc[0] = dot4(f, f, acc[0]);
-                acc[ND] = dot4(f, z, acc[ND]);
-                if (ADOT) {
-#pragma unroll
-                    for (int i = 1; i < M; ++i) acc[i] = dot4(f, xc[i][t], acc[i]);
-                }
-                if (BDOT) {
-#pragma unroll
-                    for (int j = 0; j < M; ++j) acc[M + j] = dot4(f, xn[j][t], acc[M + j]);
-                }
-            }
-        }
-        if (DOTS) {
-            constexpr int NT = (NA + 3) / 4;
-            float tot[NT];
-            wave_sums_rows<NA>(acc, tot);
-            const float fz = lane_f(tot[ND / 4], 16 * sum_row(ND));
-            if ((lane & 15) == 0) {
-                float *dr = dots + (k * NS + s) * ND;
-                const int q = lane >> 4;
-#pragma unroll
-                for (int j = 0; j < NT; ++j) {
-                    const int t = 4 * j + 2 * (q & 1) + (q >> 1);
-                    const bool used = t == 0 || (t < M ? ADOT : BDOT);
-                    if (t < ND) dr[t] = t == 0 ? tot[j] : (used ? tot[j] - fz : 0.f);
-                }
-            }
-        }
-    }
-}
-
 // A sweep over the workgroup's R rows: rows [0, RL) from LDS (loaded two
-// ahead) and, in the streamed variant (LDSW false), rows [RL, RL + Rr) from
-// the sweepers' registers and rows [RL + Rr, R) from memory at gs (loaded
-// four ahead).
-template <int M, int KS, bool LDSW, bool MAT, bool ADOT, bool BDOT, int NS = kSweepers,
-          int RR = 0>
+// ahead) and, in the streamed variant (LDSW false), rows [RL, R) from
+// memory at gs (loaded four ahead on three sweepers, two ahead on four:
+// four sweepers on 5-step blocks have no registers left for deeper loads).
+template <int M, int KS, bool LDSW, bool MAT, bool ADOT, bool BDOT, int NS = kSweepers>
 __device__ inline void sweep_rows(f4 *lw, int RL, f4 *gs, int R, int P4, int nw,
                                   const f4 (&xp)[M][KS], const f4 (&xc)[M][KS],
-                                  const f4 (&xn)[M][KS], const float *coef_prev, float *dots,
-                                  f4 (&wreg)[RR > 0 ? RR : 1][KS], int Rr) {
+                                  const f4 (&xn)[M][KS], const float *coef_prev, float *dots) {
     constexpr int ND = 2 * M;
+    constexpr int AHEAD = NS == 4 ? 2 : 4;
     pipe_sweep<M, KS, 2, true, MAT, ADOT, BDOT, NS>(lw, RL, P4, nw, xp, xc, xn, coef_prev, dots);
-    if constexpr (!LDSW) {
-        reg_sweep<M, KS, RR, MAT, ADOT, BDOT, NS>(wreg, Rr, xp, xc, xn,
-                                                  coef_prev + (size_t)RL * (M + 1),
-                                                  dots + (size_t)RL * NS * ND);
-        pipe_sweep<M, KS, 4, false, MAT, ADOT, BDOT, NS>(gs, R - RL - Rr, P4, nw, xp, xc, xn,
-                                                         coef_prev + (size_t)(RL + Rr) * (M + 1),
-                                                         dots + (size_t)(RL + Rr) * NS * ND);
-    }
+    if constexpr (!LDSW)
+        pipe_sweep<M, KS, AHEAD, false, MAT, ADOT, BDOT, NS>(gs, R - RL, P4, nw, xp, xc, xn,
+                                                         coef_prev + (size_t)RL * (M + 1),
+                                                         dots + (size_t)RL * NS * ND);
 }
 
 // ---------------------------------------------------------------- long rows
@@ -661,12 +581,10 @@ struct SampleDots {
 
 // RMAX > 0: rows too long for sample registers, swept by sweep_cols (rows
 // streamed, at most RMAX per workgroup, the first RL <= kColsLdsRows of them
-// in LDS); KS is then unused.  RR > 0 (streamed variant): the RR rows after
-// the LDS ones stay in the sweepers' registers for the whole launch, each
-// sweeper holding its slices of them, and are written back at the end.
+// in LDS); KS is then unused.
 constexpr int kColsLdsRows = 4;
 
-template <int M, int KS, bool LDSW, int RMAX = 0, int NS = kSweepers, int RR = 0>
+template <int M, int KS, bool LDSW, int RMAX = 0, int NS = kSweepers>
 __global__ __launch_bounds__(64 * (NS + 1), 1) void train_pipe_kernel(TrainArgs a) {
     static_assert(RMAX == 0 || NS == kSweepers, "the column-walk sweep runs three sweepers");
     constexpr int kBlock = 64 * (NS + 1);
@@ -706,9 +624,7 @@ __global__ __launch_bounds__(64 * (NS + 1), 1) void train_pipe_kernel(TrainArgs 
         const row_t<false> *g = rows_as<false>(gw);
         for (int e = tid; e < RL * P4; e += kBlock) lw[e] = g[e];
     }
-    // rows [RL, RL + Rr) live in the sweepers' registers (streamed variant)
-    const int Rr = (LDSW || RMAX > 0 || RR == 0) ? 0 : (R - RL < RR ? (R - RL > 0 ? R - RL : 0) : RR);
-    f4 *gs = gw + (int64_t)(RL + Rr) * P4;  // first streamed row
+    f4 *gs = gw + (int64_t)RL * P4;  // first streamed row
     const int64_t nb = (a.nsteps + M - 1) / M;
     __syncthreads();
     // The controller and the sweepers run separate loops over the blocks that
@@ -830,27 +746,14 @@ __global__ __launch_bounds__(64 * (NS + 1), 1) void train_pipe_kernel(TrainArgs 
     } else {
         StepWindow<int> own;
         own.init(a, 0);
-        f4 wreg[RR > 0 ? RR : 1][KS];
-        {
-            const int sw_ = __builtin_amdgcn_readfirstlane(wave);
-#pragma unroll
-            for (int k = 0; k < RR; ++k)
-#pragma unroll
-                for (int t = 0; t < KS; ++t) {
-                    const bool live = k < Rr && t < nw;
-                    wreg[k][t] = live ? gw[(int64_t)(RL + k) * P4 + 64 * (sw_ + NS * t) + lane]
-                                      : f4{0.f, 0.f, 0.f, 0.f};
-                }
-        }
         // Slices of the samples of the previous, current and next block.
         f4 xp[M][KS], xc[M][KS], xn[M][KS];
         load_samples<M, KS, NS>(xc, a, 0, own);
         if (nb > 1) load_samples<M, KS, NS>(xn, a, 1, own);
         // Products of the initial prototypes with block 0 (centred on its
         // first sample): f.f and f.(x_{0,i} - z), parity 1.
-        sweep_rows<M, KS, LDSW, false, true, false, NS, RR>(l.lw, RL, gs, R, P4, nw, xc, xc, xc,
-                                                         l.coef, l.dots + (size_t)l.Rp * NS * ND,
-                                                         wreg, Rr);
+        sweep_rows<M, KS, LDSW, false, true, false, NS>(l.lw, RL, gs, R, P4, nw, xc, xc, xc, l.coef,
+                                                     l.dots + (size_t)l.Rp * NS * ND);
         __syncthreads();
         for (int64_t blk = 0; blk < nb; ++blk) {
             const int par = (int)(blk & 1);
@@ -859,14 +762,14 @@ __global__ __launch_bounds__(64 * (NS + 1), 1) void train_pipe_kernel(TrainArgs 
             const bool has_next = blk + 1 < nb;
             if (blk == 0) {
                 if (has_next)
-                    sweep_rows<M, KS, LDSW, false, true, true, NS, RR>(l.lw, RL, gs, R, P4, nw, xp, xc,
-                                                                       xn, cp, dd, wreg, Rr);
+                    sweep_rows<M, KS, LDSW, false, true, true, NS>(l.lw, RL, gs, R, P4, nw, xp, xc, xn,
+                                                                   cp, dd);
             } else if (has_next) {
-                sweep_rows<M, KS, LDSW, true, true, true, NS, RR>(l.lw, RL, gs, R, P4, nw, xp, xc, xn,
-                                                                  cp, dd, wreg, Rr);
+                sweep_rows<M, KS, LDSW, true, true, true, NS>(l.lw, RL, gs, R, P4, nw, xp, xc, xn, cp,
+                                                              dd);
             } else {
-                sweep_rows<M, KS, LDSW, true, false, false, NS, RR>(l.lw, RL, gs, R, P4, nw, xp, xc,
-                                                                    xn, cp, dd, wreg, Rr);
+                sweep_rows<M, KS, LDSW, true, false, false, NS>(l.lw, RL, gs, R, P4, nw, xp, xc, xn,
+                                                                cp, dd);
             }
 #pragma unroll
             for (int j = 0; j < M; ++j)
@@ -880,18 +783,9 @@ __global__ __launch_bounds__(64 * (NS + 1), 1) void train_pipe_kernel(TrainArgs 
             if (bc->abort) return;
         }
         // apply the last block's updates
-        sweep_rows<M, KS, LDSW, true, false, false, NS, RR>(
+        sweep_rows<M, KS, LDSW, true, false, false, NS>(
             l.lw, RL, gs, R, P4, nw, xp, xc, xn, l.coef + (size_t)((nb - 1) & 1) * l.Rp * (M + 1),
-            l.dots, wreg, Rr);
-        {
-            const int sw_ = __builtin_amdgcn_readfirstlane(wave);
-#pragma unroll
-            for (int k = 0; k < RR; ++k)
-#pragma unroll
-                for (int t = 0; t < KS; ++t)
-                    if (k < Rr && t < nw)
-                        gw[(int64_t)(RL + k) * P4 + 64 * (sw_ + NS * t) + lane] = wreg[k][t];
-        }
+            l.dots);
     }
     if (RL > 0) {
         __syncthreads();

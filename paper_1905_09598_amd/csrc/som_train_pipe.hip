@@ -13,12 +13,11 @@ struct PipeInstance {
     int m, ks;
     bool stream_ok;  // the streamed variant fits in registers
     PipeKernel lds;
-    DotsKernel dots;
 };
 
 template <int M, int KS, bool STREAM = true>
 constexpr PipeInstance pipe_instance() {
-    return PipeInstance{M, KS, STREAM, train_pipe_kernel<M, KS, true>, block_dots_kernel<M>};
+    return PipeInstance{M, KS, STREAM, train_pipe_kernel<M, KS, true>};
 }
 
 // (M, KS): block length and float4 slices of 64 columns per sweeper (rows of
@@ -62,13 +61,27 @@ struct ColsInstance {
 };
 const ColsInstance kCols[] = {{4, 10}};
 
-// Streamed instances on four sweepers (block length, slices per sweeper,
-// rows held in the sweepers' registers): every SIMD sweeps, the controller
-// shares the first one (som_train_pipe_stream.hip).
+// Streamed instances on four sweepers (block length, slices per sweeper):
+// every SIMD sweeps, the controller shares the first one
+// (som_train_pipe_stream.hip).  Five steps a block: on the 100 x 100 map at
+// d = 2048, 5.04 us per step with four and 4.35 with five (prefetch two rows
+// ahead); six steps spill registers and measured 4.71.
 struct Wide {
-    int m, ks, rr;
+    int m, ks;
 };
-const Wide kWide[] = {{4, 2, kWideRegRows}};
+const Wide kWide[] = {{5, 2}};
+
+// The prepass kernel of the block's sample dot products, by block length.
+DotsKernel block_dots_for(int m) {
+    switch (m) {
+    case 2: return block_dots_kernel<2>;
+    case 4: return block_dots_kernel<4>;
+    case 5: return block_dots_kernel<5>;
+    case 6: return block_dots_kernel<6>;
+    case 8: return block_dots_kernel<8>;
+    default: return nullptr;
+    }
+}
 
 // Measured exchange latency of the pipelined kernel (multi-poll, per-XCD
 // replicated slots) by grid size, in microseconds.
@@ -150,10 +163,7 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
     // on its SIMD).  Only where rows are streamed (unless four sweepers are
     // asked for): with every row in LDS the LDS-resident kernel, whose
     // exchanges keep four polls in flight, measured faster (20 x 20 map,
-    // d = 2000, 64 workgroups: 1.29 against 1.74 us per step).  The first
-    // wi.rr rows past the LDS ones stay in the sweepers' registers for the
-    // whole launch (100 x 100 map, d = 2048: 5.04 -> 4.81 us per step with
-    // two), and only the rest stream.
+    // d = 2000, 64 workgroups: 1.29 against 1.74 us per step).
     for (const Wide &wi : kWide) {
         const int ks4 = (nsl + 3) / 4;
         if (wi.ks != ks4 || a.variant == 1 || a.sweepers == 3 ||
@@ -169,12 +179,10 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                 rl = (int)(fit < rmax ? fit : rmax);
                 if (a.lds_rows >= 0) rl = a.lds_rows < rl ? a.lds_rows : rl;
             }
-            // rows past the LDS ones: up to wi.rr in registers, the rest streamed
-            const int rs = rmax - rl - wi.rr > 0 ? rmax - rl - wi.rr : 0;
             if (rmax <= 64 && base <= (size_t)max_lds && (rl < rmax || a.sweepers == 4)) {
                 const double row_us = 1.12 * (ks4 * (0.027 * wi.m + 0.0395) + 0.012 * wi.m + 0.0665);
-                const double blk_us = rmax * row_us + rs * 0.05 + 0.5 + 0.15 * wi.m;
-                const double mem_us = rs * P4 * 32.0 / (8e6 / gg);
+                const double blk_us = rmax * row_us + (rmax - rl) * 0.05 + 0.5 + 0.15 * wi.m;
+                const double mem_us = (rmax - rl) * P4 * 32.0 / (8e6 / gg);
                 const double sweep = (blk_us > mem_us ? blk_us : mem_us) / wi.m;
                 const double ctl = pipe_exchange_us(gg) + 0.03 * wi.m + 0.36 / wi.m;
                 const double t = sweep > ctl ? sweep : ctl;
@@ -287,9 +295,7 @@ hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStrea
     if (plan.cols_rmax > 0) {
         // long rows: the column-walk sweep (its prepass is the same)
         PipeKernel fn = pipe_cols_kernel(plan.block_m, plan.cols_rmax);
-        DotsKernel dots = nullptr;
-        for (const PipeInstance &p : kPipe)
-            if (p.m == plan.block_m) dots = p.dots;
+        DotsKernel dots = block_dots_for(plan.block_m);
         if (!fn || !dots || !a.block_dots || P4 % 64 != 0 || a.xld != a.ld ||
             (a.N + plan.grid - 1) / plan.grid > plan.cols_rmax || plan.variant != 4 ||
             plan.lds_rows > kColsLdsRows)
@@ -309,9 +315,7 @@ hipError_t launch_train_pipe(const TrainArgs &a, const TrainPlan &plan, hipStrea
     }
     const int ns = plan.block / 64 - 1;
     if (ns != 3 && ns != 4) return hipErrorInvalidValue;
-    DotsKernel dots = nullptr;
-    for (const PipeInstance &p : kPipe)
-        if (p.m == plan.block_m) dots = p.dots;
+    DotsKernel dots = block_dots_for(plan.block_m);
     const PipeInstance *pi = pipe_for(plan.block_m, plan.kslots);
     PipeKernel fn = plan.variant == 3 ? (pi && ns == 3 ? pi->lds : nullptr)
                                       : pipe_stream_kernel(plan.block_m, plan.kslots, ns);

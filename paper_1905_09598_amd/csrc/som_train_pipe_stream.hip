@@ -14,12 +14,12 @@ PipeKernel pipe_stream_kernel(int m, int ks, int ns) {
     };
     // The shapes of the LDS-resident table whose sample registers leave
     // room for streamed rows (not KS = 7), on three sweepers; and one on
-    // four sweepers (rows of 512 float4: two slices each).
+    // four sweepers (5-step blocks, rows of 512 float4: two slices each).
     static const Entry kStream[] = {
         {8, 1, 3, train_pipe_kernel<8, 1, false>}, {4, 1, 3, train_pipe_kernel<4, 1, false>},
         {4, 2, 3, train_pipe_kernel<4, 2, false>}, {4, 3, 3, train_pipe_kernel<4, 3, false>},
         {2, 3, 3, train_pipe_kernel<2, 3, false>}, {2, 4, 3, train_pipe_kernel<2, 4, false>},
-        {4, 2, 4, train_pipe_kernel<4, 2, false, 0, 4, kWideRegRows>},
+        {5, 2, 4, train_pipe_kernel<5, 2, false, 0, 4>},
     };
     for (const Entry &e : kStream)
         if (e.m == m && e.ks == ks && e.ns == ns) return e.fn;

@@ -577,10 +577,10 @@ def test_large_maps_at_small_d_follow_the_oracle(side):
     _train_vs_oracle(side, side, 64, 150, 1)
 
 
-# The streamed pipelined kernel on four sweeper waves (plan block 320):
-# rows of 512 float4, two slices per sweeper (one for the last sweeper when
-# d leaves seven), ragged row counts, 0 to all rows in LDS; and the same
-# shapes forced onto three sweepers.
+# The streamed pipelined kernel on four sweeper waves (plan block 320,
+# blocks of five steps): rows of 512 float4, two slices per sweeper (one for
+# the last sweeper when d leaves seven), ragged row counts, 0 to all rows in
+# LDS; and the same shapes forced onto three sweepers.
 @pytest.mark.parametrize("rows,cols,d,n,epochs,grid", [
     (9, 50, 2048, 40, 1, 0),     # 2 units per workgroup at the planner's grid
     (11, 12, 2048, 41, 2, 8),    # 16-17 rows per workgroup, partial last block
@@ -601,6 +601,8 @@ def test_streamed_pipelined_sweeper_counts_follow_the_oracle(rows, cols, d, n, e
     say("streamed sweepers", sweepers, rows, cols, d, n, epochs, "grid", grid, "lds_rows", lds_rows)
     plan = _train_vs_oracle(rows, cols, d, n, epochs)
     assert plan["variant"] == 2 and plan["block"] == 64 * (int(sweepers) + 1)
+    if sweepers == "4":
+        assert plan["block_steps"] == 5
 
 
 # Rows too long for the pipelined kernel's sample registers, on its

@@ -22,7 +22,7 @@ pytestmark = pytest.mark.gpu
     (1, 3, 64, 4, 256),     # 20x20, d = 2000
     (2, 3, 256, 2, 256),    # 30x30, d = 5000
     (3, 4, 256, 4, 256),    # 50x50, d = 10000: pipelined, column walk over streamed rows
-    (4, 2, 256, 4, 320),    # 100x100, d = 2048: pipelined, streamed rows, four sweepers
+    (4, 2, 256, 5, 320),    # 100x100, d = 2048: pipelined, streamed rows, four sweepers
 ])
 def test_workload_launch_shapes(ci, variant, grid, block_steps, block, monkeypatch):
     for var in ("SOM_TRAIN_VARIANT", "SOM_TRAIN_GRID", "SOM_TRAIN_BLOCK_M", "SOM_TRAIN_LDS_ROWS",
