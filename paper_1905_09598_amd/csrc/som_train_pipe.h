@@ -387,15 +387,22 @@ __device__ inline void sweep_cols(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, 
     for (int r = 0; r < RMAX; ++r)
 #pragma unroll
         for (int t = 0; t < NA; ++t) acc[r][t] = 0.f;
-    // The rows' update coefficients, in registers for the whole pass: read
-    // from LDS per row and slice, each read's wait would also wait for the
-    // LDS rows in flight.
+    // The rows' update coefficients, as wave-uniform scalars for the whole
+    // pass: read from LDS per row and slice, each read's wait would also
+    // wait for the LDS rows in flight, and held in vector registers they
+    // take RMAX (M + 1) of them per lane, which kept blocks longer than 4
+    // steps from fitting beside the double-buffered slices.  (What does not
+    // fit in scalar registers the compiler keeps in lanes of a few vector
+    // registers, one read-lane per use.)
     float cf[RMAX][M + 1];
     if (MAT) {
 #pragma unroll
         for (int r = 0; r < RMAX; ++r)
 #pragma unroll
-            for (int i = 0; i <= M; ++i) cf[r][i] = coef_prev[(r < R ? r : 0) * (M + 1) + i];
+            for (int i = 0; i <= M; ++i)
+                cf[r][i] = __builtin_bit_cast(
+                    float, __builtin_amdgcn_readfirstlane(
+                               __builtin_bit_cast(int, coef_prev[(r < R ? r : 0) * (M + 1) + i])));
     }
     const float *xprev[M], *xcur[M], *xnext[M];
 #pragma unroll

@@ -55,11 +55,13 @@ size_t pipe_lds_bytes(int m, int rmax, int64_t P4, bool ldsw, bool cols = false,
 }
 
 // Long-row (column-walk) instances: block length and row bound per
-// workgroup (som_train_pipe_stream.hip).
+// workgroup (som_train_pipe_stream.hip).  Six steps a block: on the 50 x 50
+// map at d = 10000, 8.51 us per step with four, 7.48 with five and 6.89
+// with six; seven spill registers and measured 8.07.
 struct ColsInstance {
     int m, rmax;
 };
-const ColsInstance kCols[] = {{4, 10}};
+const ColsInstance kCols[] = {{6, 10}};
 
 // Streamed instances on four sweepers (block length, slices per sweeper):
 // every SIMD sweeps, the controller shares the first one
@@ -202,12 +204,12 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
     // Rows too long for any instance above (their sample slices would not
     // fit in registers): the column-walk sweep, rows streamed with the first
     // few kept in LDS, when the workgroups own few enough rows.  Cost:
-    // about 0.128 us per row and slice of 64 float4 per sweeper (15 VALU
-    // operations per element and block, and the loop's overhead), 0.07 us
-    // per row for the lane sums, 0.5 us of hand-over per block, and at least
-    // the streamed rows' read and write at the workgroup's share of 6.8 TB/s
-    // (the in-place stream rate of a MALL-resident footprint); the
-    // controller as above.
+    // about 0.0085 (3 M + 3) us per row and slice of 64 float4 per sweeper
+    // (3 M + 2 VALU operations per element and block, and the loop's
+    // overhead), 0.07 us per row for the lane sums, 0.5 us of hand-over per
+    // block, and at least the streamed rows' read and write at the
+    // workgroup's share of 6.8 TB/s (the in-place stream rate of a
+    // MALL-resident footprint); the controller as above.
     const bool no_rows_instance = best >= 1e300;
     for (const ColsInstance &ci : kCols) {
         if (!no_rows_instance || a.variant == 1) break;
@@ -221,7 +223,7 @@ double plan_train_pipe(const TrainArgs &a, int num_cus, int max_lds, TrainPlan *
                 if (fit > kColsLdsRows) fit = kColsLdsRows;
                 int rl = (int)(fit < rmax ? fit : rmax);
                 if (a.lds_rows >= 0) rl = a.lds_rows < rl ? a.lds_rows : rl;
-                const double blk_us = rmax * (ks_need * 0.128 + 0.07) + 0.5;
+                const double blk_us = rmax * (ks_need * 0.0085 * (3 * ci.m + 3) + 0.07) + 0.5;
                 const double mem_us = (rmax - rl) * P4 * 32.0 / (6.8e6 / gg);
                 const double sweep = (blk_us > mem_us ? blk_us : mem_us) / ci.m;
                 const double ctl = pipe_exchange_us(gg) + 0.03 * ci.m + 0.36 / ci.m;
