@@ -628,6 +628,27 @@ def test_long_rows_pipelined_follow_the_oracle(rows, cols, d, n, epochs, grid, l
     assert plan["variant"] == 4 and plan["grid"] == grid
 
 
+# Runs shorter than one block, one block exactly, and one block plus one
+# step, on the two kernels with the longest blocks: the four-sweeper
+# streamed kernel (5 steps a block) and the column walk (6).  The sample
+# products' prepass, the controller's exchanges and the sweepers' last
+# update must all stop at the last real step.
+@pytest.mark.parametrize("steps", [1, 2, 4, 5, 6, 7])
+@pytest.mark.parametrize("rows,cols,d,grid,sweepers,block_steps", [
+    (11, 12, 2048, 8, "4", 5),   # four sweepers, streamed rows
+    (5, 4, 6000, 3, "", 6),      # column walk
+])
+def test_runs_shorter_than_a_block_follow_the_oracle(rows, cols, d, grid, sweepers, block_steps,
+                                                     steps, monkeypatch):
+    monkeypatch.setenv("SOM_TRAIN_VARIANT", "4")
+    monkeypatch.setenv("SOM_TRAIN_GRID", str(grid))
+    if sweepers:
+        monkeypatch.setenv("SOM_TRAIN_SWEEPERS", sweepers)
+    say("short run", rows, cols, d, "steps", steps, "grid", grid)
+    plan = _train_vs_oracle(rows, cols, d, steps, 1)
+    assert plan["block_steps"] == block_steps and plan["grid"] == grid
+
+
 def test_long_rows_pipelined_hexagonal_and_schedule_edges(monkeypatch):
     # the column-walk sweep on a hexagonal lattice, then a unit rate with a
     # zero radius, which must copy each sample exactly into its BMU
