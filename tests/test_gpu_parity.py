@@ -582,7 +582,7 @@ def test_large_maps_at_small_d_follow_the_oracle(side):
 # the last sweeper when d leaves seven), ragged row counts, 0 to all rows in
 # LDS; and the same shapes forced onto three sweepers.
 @pytest.mark.parametrize("rows,cols,d,n,epochs,grid", [
-    (9, 50, 2048, 40, 1, 0),     # 2 units per workgroup at the planner's grid
+    (9, 50, 2048, 40, 1, 0),     # the planner's grid: 64 (four sweepers) or 128 workgroups
     (11, 12, 2048, 41, 2, 8),    # 16-17 rows per workgroup, partial last block
     (20, 13, 1500, 61, 2, 8),    # 375 float4 of 512: the last slices partly zero
     (20, 20, 1100, 17, 1, 8),    # 50 rows per workgroup, d = 1100 (row pitch 2048)
@@ -591,8 +591,8 @@ def test_large_maps_at_small_d_follow_the_oracle(side):
 @pytest.mark.parametrize("sweepers", ["4", "3"])
 def test_streamed_pipelined_sweeper_counts_follow_the_oracle(rows, cols, d, n, epochs, grid,
                                                              lds_rows, sweepers, monkeypatch):
-    if rows * cols / max(grid, 1) > 64:
-        pytest.skip("more than 64 units per workgroup")
+    if grid and rows * cols / grid > 64:
+        pytest.skip("more than 64 units per workgroup")   # (the planner's grid never has)
     monkeypatch.setenv("SOM_TRAIN_VARIANT", "4")
     monkeypatch.setenv("SOM_TRAIN_SWEEPERS", sweepers)
     monkeypatch.setenv("SOM_TRAIN_LDS_ROWS", lds_rows)
