@@ -12,14 +12,15 @@ three families:
 
 Each case trains on the GPU and must follow the oracle's BMU sequence until
 an oracle near tie (relative top-two gap <= 1e-4), with weights within
-1e-4 where the whole sequence agrees."""
+1e-4 where the whole sequence agrees.  A fourth family draws evaluation
+shapes (up to 80 x 80 units, 3000 samples) for the batched BMU, QE and TE."""
 import numpy as np
 import pytest
 
 import oracle
 import paper_1905_09598_amd as som
 import workloads
-from gpu_util import dev, say
+from gpu_util import dev, rel_gap, say
 
 pytestmark = pytest.mark.gpu
 
@@ -116,3 +117,56 @@ def test_random_shape_follows_the_oracle(family, seed, case, monkeypatch):
         say(f"  plan {plan}: identical BMUs for {k}/{len(tr)} steps")
         assert len(Ds) > 1 and (Ds[1] - Ds[0]) / Ds[0] <= GAP, "divergence without a near tie"
     m.close()
+
+
+# ---------------------------------------------------------------- batched BMU
+def _bmu_cases(seed, count):
+    """Random (rows, cols, d, n, topology): up to 80 x 80 units, d at the
+    slicing edges or random, n up to 3000, with n N d kept within what the
+    oracle evaluates in about a second."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(count):
+        rows, cols = int(rng.integers(1, 81)), int(rng.integers(1, 81))
+        d = int(rng.choice(D_EDGE)) if rng.random() < 0.5 else int(rng.integers(1, 12001))
+        n = int(rng.integers(1, 3001))
+        while n > 1 and n * rows * cols * d > 1.5e9:
+            n //= 2
+        out.append((rows, cols, d, n, som.HEX if rng.random() < 0.3 else som.RECT))
+    return out
+
+
+@pytest.mark.parametrize("case", _bmu_cases(21, 24), ids=[f"bmu-{i}" for i in range(24)])
+def test_random_shape_batched_bmu_and_quality_follow_the_oracle(case):
+    """BMUs and second BMUs where the oracle's gaps are clear, the BMU
+    distance everywhere, QE to 1e-5 and the TE count up to the samples whose
+    BMU or second BMU is an oracle near tie, through som_bmu2 and
+    som_evaluate (the fused or split candidate search the planner picks)."""
+    rows, cols, d, n, topology = case
+    say("random bmu", rows, cols, d, n, topology)
+    k0 = rows * 7919 + cols * 104729 + d + n
+    X = workloads.gaussian_mixture(n, d, 8, 0.2, seed=k0 % 100003)
+    W = workloads.random_weights(rows * cols, d, k0 % 65521, -1.0, 1.0)
+    m = som.Map(rows, cols, d, seed=0, topology=topology)
+    m.weights = dev(W)
+    Xd = dev(X)
+    idx, idx2, d1 = (t.cpu().numpy() for t in m.bmu(Xd, second=True))
+    _, qe, te = m.evaluate(Xd, with_bmu=False)
+    m.close()
+    W64 = W.astype(np.float64)
+    ev = oracle.evaluate(W64, rows, cols, X, topology=topology)
+    D = np.stack([oracle.distances(W64, X[i]) for i in range(n)])
+    Ds = np.sort(D, axis=1)
+    g1 = rel_gap(Ds[:, 0], Ds[:, 1]) if D.shape[1] > 1 else np.full(n, np.inf)
+    g2 = rel_gap(Ds[:, 1], Ds[:, 2]) if D.shape[1] > 2 else np.full(n, np.inf)
+    sure = g1 > GAP
+    assert np.array_equal(idx[sure], ev["c1"][sure])
+    assert np.all(np.abs(d1 - ev["d1"]) <= 1e-5 * np.maximum(ev["d1"], 1e-3) + 1e-6)
+    if rows * cols == 1:
+        assert np.all(idx2 == -1)
+    else:
+        sure2 = sure & (g2 > GAP)
+        assert np.array_equal(idx2[sure2], ev["c2"][sure2])
+    assert qe == pytest.approx(ev["qe"], rel=1e-5)
+    unsure = int(np.sum(~(sure & (g2 > GAP))))
+    assert abs(round(te * n) - round(ev["te"] * n)) <= unsure
