@@ -144,6 +144,41 @@ def test_ragged_shapes_follow_the_oracle(rows, cols, d, n, nnz_max, epochs):
     _sparse_vs_oracle(X, rows, cols, order, s, topology=som.RECT, W=W)
 
 
+def _random_csr_cases(seed, count):
+    """Random (rows, cols, d, n, nnz_max, epochs, topology): up to 40 x 40
+    units (one to 25 workgroups of 64), d from 1 to 20000 with the
+    64-feature edges over-weighted, up to the kernel's 64 non-zeros a row."""
+    rng = np.random.default_rng(seed)
+    edges = [1, 2, 5, 63, 64, 65, 127, 128, 129, 4095, 4096, 4097, 20000]
+    out = []
+    for _ in range(count):
+        rows, cols = int(rng.integers(1, 41)), int(rng.integers(1, 41))
+        d = int(rng.choice(edges)) if rng.random() < 0.4 else int(rng.integers(1, 20001))
+        out.append((rows, cols, d, int(rng.integers(1, 61)), int(rng.integers(1, 65)),
+                    int(rng.integers(1, 4)), som.HEX if rng.random() < 0.3 else som.RECT))
+    return out
+
+
+@pytest.mark.parametrize("case", _random_csr_cases(31, 16),
+                         ids=[f"csr-{i}" for i in range(16)])
+def test_random_csr_shapes_follow_the_oracle(case):
+    rows, cols, d, n, nnz_max, epochs, topology = case
+    say("random csr", rows, cols, d, n, nnz_max, epochs, topology)
+    rng = np.random.default_rng(rows * 7919 + cols * 104729 + d)
+    X = np.zeros((n, d), np.float32)
+    for i in range(n):
+        k = 0 if rng.random() < 0.08 else int(rng.integers(1, nnz_max + 1))   # some empty rows
+        j = rng.choice(d, size=min(k, d), replace=False)
+        X[i, j] = rng.random(j.size).astype(np.float32) + 0.05
+        nrm = np.linalg.norm(X[i])
+        if nrm > 0:
+            X[i] /= nrm
+    order = workloads.epoch_orders(n, epochs, int(rng.integers(1000)))
+    s = oracle.schedule(0.4, 0.02, max(rows, cols) / 2.0, 0.5)
+    W = workloads.random_weights(rows * cols, d, int(rng.integers(1000)), 0.0, 0.2)
+    _sparse_vs_oracle(X, rows, cols, order, s, topology=topology, W=W)
+
+
 def test_rescaling_of_the_lazy_scale_follows_the_oracle():
     # sigma = inf: every unit gets h = lr whatever the BMU, so the trained
     # map does not depend on BMU decisions.  lr = 0.9 divides the scale by
