@@ -309,26 +309,39 @@ def batch_sigma(e: int, epochs: int, sigma0: float, sigma1: float,
     return schedule_at(e, epochs, s)[1]
 
 
+def batch_update(W: np.ndarray, rows: int, cols: int, X: np.ndarray, c: np.ndarray,
+                 sigma: float, topology: int = RECT) -> np.ndarray:
+    """One batch-map update given every sample's BMU c (a float64 copy of W
+    is returned): unit u becomes sum_k h(u, k) S_k / sum_k h(u, k) n_k, with
+    S_k and n_k the sum and count of the samples whose BMU is k; a unit whose
+    denominator is 0 keeps its prototype."""
+    W = np.array(W, dtype=np.float64, order="C", copy=True)
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    c = np.asarray(c, dtype=np.int64)
+    N = rows * cols
+    H = np.stack([neighbourhood(rows, cols, topology, k, 1.0, sigma)
+                  for k in range(N)], axis=1)          # H[u, k] = h(u, k)
+    S = np.zeros((N, X.shape[1]), dtype=np.float64)
+    np.add.at(S, c, X.astype(np.float64))
+    cnt = np.bincount(c, minlength=N).astype(np.float64)
+    num = H @ S
+    den = H @ cnt
+    keep = den > 0
+    W[keep] = num[keep] / den[keep, None]
+    return W
+
+
 def train_batch(W: np.ndarray, rows: int, cols: int, X: np.ndarray, epochs: int,
                 sigma0: float, sigma1: float, sigma_decay: int = EXPONENTIAL,
                 topology: int = RECT, nthreads: Optional[int] = None, trace: bool = False):
     """`epochs` batch epochs from W (float64 copy); returns (W, BMUs per epoch)."""
     W = np.array(W, dtype=np.float64, order="C", copy=True)
     X = np.ascontiguousarray(X, dtype=np.float32)
-    N = rows * cols
     bmus = []
     for e in range(epochs):
         sigma = batch_sigma(e, epochs, sigma0, sigma1, sigma_decay)
         c = evaluate(W, rows, cols, X, topology=topology, nthreads=nthreads)["c1"]
         if trace:
             bmus.append(c)
-        H = np.stack([neighbourhood(rows, cols, topology, k, 1.0, sigma)
-                      for k in range(N)], axis=1)          # H[u, k] = h(u, k)
-        S = np.zeros((N, X.shape[1]), dtype=np.float64)
-        np.add.at(S, c, X.astype(np.float64))
-        cnt = np.bincount(c, minlength=N).astype(np.float64)
-        num = H @ S
-        den = H @ cnt
-        keep = den > 0
-        W[keep] = num[keep] / den[keep, None]
+        W = batch_update(W, rows, cols, X, c, sigma, topology)
     return W, bmus
