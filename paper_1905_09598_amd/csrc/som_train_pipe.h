@@ -353,8 +353,10 @@ __device__ inline void block_indices(int (&idx)[M], const TrainArgs &a, int64_t 
 // samples are loaded while the current one is computed.  Arguments as
 // sweep_rows; ip, ic, inx are the sample indices of the previous, current
 // and next block; dummy is this sweeper's 64-float4 area for the LDS writes
-// of streamed rows.
-template <int M, int RMAX, int RLMAX, bool MAT, bool ADOT, bool BDOT>
+// of streamed rows.  This call walks the window of rows [R0, R0 + RMAX) of
+// the workgroup's R (sweep_cols_split below walks all of them in windows);
+// LDS rows must lie in a window with R0 = 0.
+template <int M, int RMAX, int RLMAX, bool MAT, bool ADOT, bool BDOT, int R0 = 0>
 __device__ inline void sweep_cols(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, int R, int P4,
                                   int nw, const int (&ip)[M], const int (&ic)[M],
                                   const int (&inx)[M], const float *coef_prev, float *dots,
@@ -367,7 +369,8 @@ __device__ inline void sweep_cols(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, 
     // every row offset with it.
     const int s = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     nw = __builtin_amdgcn_readfirstlane(nw);
-    if (R <= 0 || nw <= 0) return;
+    static_assert(R0 == 0 || RLMAX == 0, "LDS rows lie in the first window");
+    if (R <= R0 || nw <= 0) return;
     row_t<true> *lw = rows_as<true>(lw_p);
     row_t<true> *dummy = rows_as<true>(dummy_p);
     const int lane = threadIdx.x & 63;
@@ -375,12 +378,15 @@ __device__ inline void sweep_cols(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, 
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         gs, (short)0, RS > 0 ? RS * P4 * 16 : 0, 0x00020000);
     constexpr int kOutside = 1 << 30;  // bytes, beyond any sweep's rows
-    // Streamed row r's byte offset (a scalar per row): LDS rows and rows
-    // past R read zeros and drop their stores.
+    // Streamed row R0 + r's byte offset (a scalar per row): LDS rows and
+    // rows past R read zeros and drop their stores.
     int soff[RMAX];
 #pragma unroll
-    for (int r = 0; r < RMAX; ++r)
-        soff[r] = __builtin_amdgcn_readfirstlane((r >= RL && r < R) ? (r - RL) * P4 * 16 : kOutside);
+    for (int r = 0; r < RMAX; ++r) {
+        const int rg = R0 + r;
+        soff[r] = __builtin_amdgcn_readfirstlane((rg >= RL && rg < R) ? (rg - RL) * P4 * 16
+                                                                      : kOutside);
+    }
     const auto row_off = [&](int r) { return soff[r]; };
     float acc[RMAX][NA];
 #pragma unroll
@@ -401,8 +407,8 @@ __device__ inline void sweep_cols(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, 
 #pragma unroll
             for (int i = 0; i <= M; ++i)
                 cf[r][i] = __builtin_bit_cast(
-                    float, __builtin_amdgcn_readfirstlane(
-                               __builtin_bit_cast(int, coef_prev[(r < R ? r : 0) * (M + 1) + i])));
+                    float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(
+                               int, coef_prev[(R0 + r < R ? R0 + r : 0) * (M + 1) + i])));
     }
     const float *xprev[M], *xcur[M], *xnext[M];
 #pragma unroll
@@ -423,7 +429,7 @@ __device__ inline void sweep_cols(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, 
     // make the compiler wait for it on the spot.
     struct Slice {
         f4 g[RMAX];   // streamed rows
-        f4 l[RLMAX];  // LDS rows
+        f4 l[RLMAX > 0 ? RLMAX : 1];  // LDS rows
         f4 x[3][M];   // samples: previous, current, next block
     };
     // (a 32-bit unsigned byte offset from a scalar row base: one address
@@ -510,12 +516,12 @@ __device__ inline void sweep_cols(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, 
         constexpr int NT = (NA + 3) / 4;
 #pragma unroll
         for (int r = 0; r < RMAX; ++r) {
-            if (r < R) {
+            if (R0 + r < R) {
                 float tot[NT];
                 wave_sums_rows<NA>(acc[r], tot);
                 const float fz = lane_f(tot[ND / 4], 16 * sum_row(ND));
                 if ((lane & 15) == 0) {
-                    float *dr = dots + (r * kSweepers + s) * ND;
+                    float *dr = dots + ((R0 + r) * kSweepers + s) * ND;
                     const int qq = lane >> 4;
 #pragma unroll
                     for (int j = 0; j < NT; ++j) {
@@ -527,6 +533,25 @@ __device__ inline void sweep_cols(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, 
             }
         }
     }
+}
+
+// The column walk over all of a workgroup's rows in two windows, the first
+// holding the LDS rows: each window keeps only its rows' running products
+// and coefficients live, so the registers they free hold longer blocks'
+// samples instead.  Every row's products sum over the slices in the same
+// order as in a single pass; the samples' slices are read once per window
+// (from L2).
+template <int M, int RMAX, int RLMAX, bool MAT, bool ADOT, bool BDOT>
+__device__ inline void sweep_cols_split(const TrainArgs &a, f4 *lw_p, int RL, f4 *gs, int R,
+                                        int P4, int nw, const int (&ip)[M], const int (&ic)[M],
+                                        const int (&inx)[M], const float *coef_prev, float *dots,
+                                        f4 *dummy_p) {
+    constexpr int H = (RMAX + 1) / 2;
+    static_assert(RLMAX <= H, "the LDS rows lie in the first window");
+    sweep_cols<M, H, RLMAX, MAT, ADOT, BDOT, 0>(a, lw_p, RL, gs, R, P4, nw, ip, ic, inx,
+                                                coef_prev, dots, dummy_p);
+    sweep_cols<M, RMAX - H, 0, MAT, ADOT, BDOT, H>(a, lw_p, RL, gs, R, P4, nw, ip, ic, inx,
+                                                   coef_prev, dots, dummy_p);
 }
 
 // ---------------------------------------------------------------- controller
@@ -717,7 +742,7 @@ __global__ __launch_bounds__(64 * (NS + 1), 1) void train_pipe_kernel(TrainArgs 
         for (int j = 0; j < M; ++j) inx[j] = ip[j] = ic[j];
         if (nb > 1) block_indices<M>(inx, a, 1, own);
         f4 *dm = l.dummy;
-        sweep_cols<M, RMAX, kColsLdsRows, false, true, false>(
+        sweep_cols_split<M, RMAX, kColsLdsRows, false, true, false>(
             a, l.lw, RL, gs, R, P4, nw, ic, ic, ic, l.coef, l.dots + (size_t)l.Rp * kSweepers * ND,
             dm);
         __syncthreads();
@@ -728,14 +753,14 @@ __global__ __launch_bounds__(64 * (NS + 1), 1) void train_pipe_kernel(TrainArgs 
             const bool has_next = blk + 1 < nb;
             if (blk == 0) {
                 if (has_next)
-                    sweep_cols<M, RMAX, kColsLdsRows, false, true, true>(a, l.lw, RL, gs, R, P4, nw,
-                                                                         ip, ic, inx, cp, dd, dm);
+                    sweep_cols_split<M, RMAX, kColsLdsRows, false, true, true>(
+                        a, l.lw, RL, gs, R, P4, nw, ip, ic, inx, cp, dd, dm);
             } else if (has_next) {
-                sweep_cols<M, RMAX, kColsLdsRows, true, true, true>(a, l.lw, RL, gs, R, P4, nw, ip,
-                                                                    ic, inx, cp, dd, dm);
+                sweep_cols_split<M, RMAX, kColsLdsRows, true, true, true>(
+                    a, l.lw, RL, gs, R, P4, nw, ip, ic, inx, cp, dd, dm);
             } else {
-                sweep_cols<M, RMAX, kColsLdsRows, true, false, false>(a, l.lw, RL, gs, R, P4, nw,
-                                                                      ip, ic, inx, cp, dd, dm);
+                sweep_cols_split<M, RMAX, kColsLdsRows, true, false, false>(
+                    a, l.lw, RL, gs, R, P4, nw, ip, ic, inx, cp, dd, dm);
             }
 #pragma unroll
             for (int j = 0; j < M; ++j) {
@@ -747,7 +772,7 @@ __global__ __launch_bounds__(64 * (NS + 1), 1) void train_pipe_kernel(TrainArgs 
             if (bc->abort) return;
         }
         // apply the last block's updates
-        sweep_cols<M, RMAX, kColsLdsRows, true, false, false>(
+        sweep_cols_split<M, RMAX, kColsLdsRows, true, false, false>(
             a, l.lw, RL, gs, R, P4, nw, ip, ic, inx,
             l.coef + (size_t)((nb - 1) & 1) * l.Rp * (M + 1), l.dots, dm);
     } else {

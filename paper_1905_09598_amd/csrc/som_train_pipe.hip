@@ -55,13 +55,15 @@ size_t pipe_lds_bytes(int m, int rmax, int64_t P4, bool ldsw, bool cols = false,
 }
 
 // Long-row (column-walk) instances: block length and row bound per
-// workgroup (som_train_pipe_stream.hip).  Six steps a block: on the 50 x 50
-// map at d = 10000, 8.51 us per step with four, 7.48 with five and 6.89
-// with six; seven spill registers and measured 8.07.
+// workgroup (som_train_pipe_stream.hip).  Eight steps a block, the rows
+// walked in two windows: on the 50 x 50 map at d = 10000, 8.51 us per step
+// with four steps in one pass, 6.89 with six, 6.54 with six in two windows
+// and 6.18 with eight (ten spill registers: 6.62; three windows reread the
+// samples once more: 6.34 with twelve).
 struct ColsInstance {
     int m, rmax;
 };
-const ColsInstance kCols[] = {{6, 10}};
+const ColsInstance kCols[] = {{8, 10}};
 
 // Streamed instances on four sweepers (block length, slices per sweeper):
 // every SIMD sweeps, the controller shares the first one

@@ -32,7 +32,7 @@ PipeKernel pipe_cols_kernel(int m, int rmax) {
         PipeKernel fn;
     };
     static const Entry kCols[] = {
-        {6, 10, train_pipe_kernel<6, 1, false, 10>},
+        {8, 10, train_pipe_kernel<8, 1, false, 10>},
     };
     for (const Entry &e : kCols)
         if (e.m == m && e.rmax == rmax) return e.fn;

@@ -630,13 +630,13 @@ def test_long_rows_pipelined_follow_the_oracle(rows, cols, d, n, epochs, grid, l
 
 # Runs shorter than one block, one block exactly, and one block plus one
 # step, on the two kernels with the longest blocks: the four-sweeper
-# streamed kernel (5 steps a block) and the column walk (6).  The sample
+# streamed kernel (5 steps a block) and the column walk (8).  The sample
 # products' prepass, the controller's exchanges and the sweepers' last
 # update must all stop at the last real step.
-@pytest.mark.parametrize("steps", [1, 2, 4, 5, 6, 7])
+@pytest.mark.parametrize("steps", [1, 2, 4, 5, 6, 7, 8, 9])
 @pytest.mark.parametrize("rows,cols,d,grid,sweepers,block_steps", [
     (11, 12, 2048, 8, "4", 5),   # four sweepers, streamed rows
-    (5, 4, 6000, 3, "", 6),      # column walk
+    (5, 4, 6000, 3, "", 8),      # column walk (two windows of rows)
 ])
 def test_runs_shorter_than_a_block_follow_the_oracle(rows, cols, d, grid, sweepers, block_steps,
                                                      steps, monkeypatch):

@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
     (0, 3, 8, 4, 256),      # 10x10, d = 500: pipelined, LDS rows
     (1, 3, 64, 4, 256),     # 20x20, d = 2000
     (2, 3, 256, 2, 256),    # 30x30, d = 5000
-    (3, 4, 256, 6, 256),    # 50x50, d = 10000: pipelined, column walk over streamed rows
+    (3, 4, 256, 8, 256),    # 50x50, d = 10000: pipelined, column walk over streamed rows
     (4, 2, 256, 5, 320),    # 100x100, d = 2048: pipelined, streamed rows, four sweepers
 ])
 def test_workload_launch_shapes(ci, variant, grid, block_steps, block, monkeypatch):

@@ -8,7 +8,7 @@ three families:
   * wide: the four-sweeper streamed kernel (rows of 385-512 float4, few
     workgroups, 5-step blocks);
   * cols: the column walk (rows of 3073-16384 floats, at most 10 per
-    workgroup, 6-step blocks).
+    workgroup, 8-step blocks, two windows of rows).
 
 Each case trains on the GPU and must follow the oracle's BMU sequence until
 an oracle near tie (relative top-two gap <= 1e-4), with weights within
@@ -100,7 +100,7 @@ def test_random_shape_follows_the_oracle(family, seed, case, monkeypatch):
     if family == "wide":
         assert (plan["variant"], plan["block"], plan["block_steps"]) == (2, 320, 5)
     if family == "cols":
-        assert (plan["variant"], plan["block_steps"]) == (4, 6)
+        assert (plan["variant"], plan["block_steps"]) == (4, 8)
     trace = dev(np.full(epochs * n, -1, np.int32))
     m.train(dev(X), epochs, 0.4, 0.02, sig0, 0.5, order=dev(order), bmu_trace=trace)
     got = trace.cpu().numpy()
